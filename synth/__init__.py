@@ -1,0 +1,26 @@
+"""Seeded synthetic attention inputs shared by the oracle, the GPU tests and the bench.
+
+This package only draws and rounds numbers: it holds none of the attention method's
+arithmetic, so both sides of every parity check consume bit-identical bf16 inputs
+without sharing any code that computes attention.
+"""
+
+from .video_qkv import (
+    WORKLOADS,
+    Workload,
+    bf16_bits,
+    position_features,
+    make_random_qkv,
+    make_video_qkv,
+    workload_inputs,
+)
+
+__all__ = [
+    "WORKLOADS",
+    "Workload",
+    "bf16_bits",
+    "position_features",
+    "make_random_qkv",
+    "make_video_qkv",
+    "workload_inputs",
+]
