@@ -1,0 +1,245 @@
+"""Throughput of the DynSparse forward pass on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload wan720p]
+
+A step is one call of ``dynsparse_attn_fwd`` (recall target 0.95) over a whole
+Wan-2.2-14B-like 720p attention layer (B=1, H=40, N=75600 = 21x45x80 latent tokens,
+d=128, bf16), with the inputs already resident in HBM.  ``value`` is the effective
+(dense-equivalent) throughput 4*B*H*N^2*d / time; the same run times the library's own
+``dense_attn_fwd`` for the speedup, reports the kernel's bf16 MFMA roofline fraction on
+the work it actually issues, and times the fp64 CPU oracle on a bounded sample of the
+same layer as a reference point.  One JSON line is printed.
+
+``--sweep`` instead prints one JSON line per rule/threshold on the given workload.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "effective TFLOP/s (dense-equiv) + speedup vs own dense FA at matched recall"
+PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 MFMA
+HBM_PEAK_GBS = 8000.0
+TILE_Q, TILE_K, D = 128, 64, 128
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="wan720p")
+    ap.add_argument("--recall", type=float, default=None, help="recall target (default: workload's)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="approximate CPU budget of the oracle baseline (0 = skip)")
+    ap.add_argument("--no-dense", action="store_true", help="skip the dense timing (profiling)")
+    ap.add_argument("--sweep", action="store_true", help="one line per rule/threshold")
+    ap.add_argument("--traffic", default=None,
+                    help="JSON file with measured HBM bytes per launch of the main kernel")
+    return ap.parse_args()
+
+
+def upload(bits):
+    import numpy as np
+    import torch
+
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def time_calls(fn, steps, warmup):
+    """Average milliseconds per call, measured with events on the launch stream."""
+    import torch
+
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(steps):
+        fn()
+    end.record(stream)
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / steps
+
+
+def algorithmic_flops(stats, d=D):
+    """QK^T on every pair plus P.V on kept pairs: 2*d per valid element each."""
+    elems = int(stats[:, 2].sum())
+    skipped = int(stats[:, 3].sum())
+    return 2 * d * elems + 2 * d * (elems - skipped)
+
+
+def cpu_baseline(q, k, v, scale, lam, budget_s):
+    """Time the fp64 oracle on Q tiles of head (0, 0) for about budget_s seconds."""
+    import numpy as np
+    import oracle
+
+    try:
+        from threadpoolctl import threadpool_info
+
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    N = q.shape[2]
+    n_qt = -(-N // TILE_Q)
+    t0 = time.perf_counter()
+    oracle.rule_attention(q, k, v, scale, "dynsparse", lam, TILE_Q, TILE_K, tiles=[(0, 0, 0)])
+    per_tile = time.perf_counter() - t0
+    n = int(max(1, min(n_qt, budget_s / max(per_tile, 1e-3))))
+    picks = sorted(set(np.linspace(0, n_qt - 1, n).astype(int).tolist()))
+    tiles = [(0, 0, i) for i in picks]
+    t0 = time.perf_counter()
+    oracle.rule_attention(q, k, v, scale, "dynsparse", lam, TILE_Q, TILE_K, tiles=tiles)
+    dt = time.perf_counter() - t0
+    rows = sum(min(N, (i + 1) * TILE_Q) - i * TILE_Q for i in picks)
+    eff = 4.0 * rows * N * D / dt / 1e12
+    return {"value": eff, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{len(tiles)} of {n_qt} query tiles of head (0,0), all {-(-N // TILE_K)} "
+                      f"key tiles each, {dt:.1f} s; dense-equivalent FLOP of the sample / time"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(--gpus must be 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2606_16317_amd as dsa
+    from synth import WORKLOADS, workload_inputs
+
+    w = WORKLOADS[args.workload]
+    recall = w.recall if args.recall is None else args.recall
+    B, H, N = w.B, w.H, w.N
+    scale = 1.0 / math.sqrt(D)
+    print(f"[bench] generating {w.describe()}", file=sys.stderr, flush=True)
+    q, k, v, meta = workload_inputs(w)
+    qd, kd, vd = upload(q), upload(k), upload(v)
+    o = torch.empty_like(qd)
+    od = torch.empty_like(qd)
+    stats = torch.zeros(B * H * 4, dtype=torch.int64, device="cuda")
+    dense_stats = torch.zeros(B * H * 4, dtype=torch.int64, device="cuda")
+    dense_flop = 4.0 * B * H * N * N * D
+    lam = dsa.dsattn_lambda_from_recall(recall, N)
+
+    if args.sweep:
+        return sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop)
+
+    def step():
+        dsa.dynsparse_attn_fwd(qd, kd, vd, o, scale=scale, recall_target=recall, stats_out=stats)
+
+    print(f"[bench] dynsparse recall={recall} lambda={lam:.3f}: {args.warmup} warmup + "
+          f"{args.steps} timed steps", file=sys.stderr, flush=True)
+    ms = time_calls(step, args.steps, args.warmup)
+    st = stats.cpu().numpy().reshape(B * H, 4)
+    flop_alg = algorithmic_flops(st)
+    sp_tiles = float(st[:, 1].sum() / st[:, 0].sum())
+    sp_elems = float(st[:, 3].sum() / st[:, 2].sum())
+
+    dense_ms = None
+    rel_l2 = None
+    if not args.no_dense:
+        print("[bench] dense reference timing", file=sys.stderr, flush=True)
+
+        def dstep():
+            dsa.dense_attn_fwd(qd, kd, vd, od, scale=scale, stats_out=dense_stats)
+
+        dense_ms = time_calls(dstep, args.steps, args.warmup)
+        diff = (o.float() - od.float()).pow(2).sum().sqrt()
+        rel_l2 = float(diff / od.float().pow(2).sum().sqrt())
+
+    achieved = flop_alg / (ms * 1e-3) / 1e12
+    traffic = None
+    if args.traffic and os.path.exists(args.traffic):
+        traffic = json.load(open(args.traffic)).get("bytes_per_launch")
+    cpu = None
+    if args.cpu_seconds > 0:
+        print("[bench] cpu oracle baseline", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(q, k, v, scale, lam, args.cpu_seconds)
+
+    out = {
+        "metric": METRIC,
+        "value": dense_flop / (ms * 1e-3) / 1e12,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: Wan-2.2-14B-like 720p attention layer, "
+                               f"B={B} H={H} N={N} ({'x'.join(map(str, w.grid))}) d={D}, "
+                               f"bf16 in / fp32 accumulate, tile {TILE_Q}x{TILE_K}",
+                   "rule": "dynsparse", "recall_target": recall, "lambda": lam,
+                   "seed": w.seed},
+        "speedup_vs_dense": (dense_ms / ms) if dense_ms else None,
+        "dense_ms_per_step": dense_ms,
+        "dense_effective_tflops": (dense_flop / (dense_ms * 1e-3) / 1e12) if dense_ms else None,
+        "actual_tflops": achieved,
+        "sparsity_tiles": sp_tiles,
+        "sparsity_elems": sp_elems,
+        "rel_l2_vs_dense": rel_l2,
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
+                     "traffic": traffic},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop):
+    import torch
+
+    B, H, N = w.B, w.H, w.N
+    points = [("dense", None)] + [("dynsparse_recall", r) for r in (0.90, 0.95, 0.98, 0.99)] + \
+             [("dynsparse_lambda", l) for l in (-6.0, -8.0, -10.0)] + \
+             [("blasst", t) for t in (1e-2, 1e-3, 1e-4)]
+    dense_ms = None
+    for rule, p in points:
+        if rule == "dense":
+            fn = lambda: dsa.dense_attn_fwd(qd, kd, vd, od, scale=scale, stats_out=stats)
+        elif rule == "dynsparse_recall":
+            fn = lambda: dsa.dynsparse_attn_fwd(qd, kd, vd, o, scale=scale, recall_target=p,
+                                                stats_out=stats)
+        elif rule == "dynsparse_lambda":
+            fn = lambda: dsa.dynsparse_attn_fwd_lambda(qd, kd, vd, o, scale=scale, lam=p,
+                                                       stats_out=stats)
+        else:
+            fn = lambda: dsa.blasst_attn_fwd(qd, kd, vd, o, scale=scale, threshold=p,
+                                             stats_out=stats)
+        print(f"[sweep] {rule} {p}", file=sys.stderr, flush=True)
+        ms = time_calls(fn, args.steps, args.warmup)
+        st = stats.cpu().numpy().reshape(B * H, 4)
+        if rule == "dense":
+            dense_ms = ms
+            rel = 0.0
+        else:
+            rel = float((o.float() - od.float()).pow(2).sum().sqrt() /
+                        od.float().pow(2).sum().sqrt())
+        rec = {"workload": w.name, "rule": rule, "param": p, "ms": ms,
+               "effective_tflops": dense_flop / (ms * 1e-3) / 1e12,
+               "actual_tflops": algorithmic_flops(st) / (ms * 1e-3) / 1e12,
+               "sparsity_tiles": float(st[:, 1].sum() / st[:, 0].sum()),
+               "speedup_vs_dense": dense_ms / ms, "rel_l2_vs_dense": rel}
+        print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,234 @@
+"""Python binding of libdsattn.so (argument marshalling only).
+
+Every function here takes torch tensors that live on the GPU, checks dtype/shape/device,
+and calls the C entry point of the same name with raw device pointers and the current
+torch stream.  All arithmetic runs in the HIP kernels of the library; there is no
+fallback: if the library is missing or a call fails, a RuntimeError is raised.
+
+Tensor conventions: q, k, v, o are contiguous bf16 tensors of shape [B, H, N, 128];
+``stats_out`` is an int64 tensor of B*H*4 elements (uint64 counters
+{tiles_total, tiles_skipped, elems_total, elems_skipped} per head); ``mask_out`` is a
+uint8 tensor of B*H*ceil(N/128)*ceil(N/64) elements; ``lse_out`` a float32 tensor of
+B*H*N elements.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+LIB_NAME = "libdsattn.so"
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), LIB_NAME)
+
+TILE_Q = 128
+TILE_K = 64
+HEAD_DIM = 128
+
+RULE_DENSE = 0
+RULE_BLASST = 1
+RULE_DYNSPARSE_RECALL = 2
+RULE_DYNSPARSE_LAMBDA = 3
+
+_lib = None
+
+
+class DsAttnArgs(ctypes.Structure):
+    """Mirror of ``dsattn_args`` in include/dsattn.h."""
+
+    _fields_ = [
+        ("rule", ctypes.c_int),
+        ("param", ctypes.c_float),
+        ("q", ctypes.c_void_p),
+        ("k", ctypes.c_void_p),
+        ("v", ctypes.c_void_p),
+        ("o", ctypes.c_void_p),
+        ("B", ctypes.c_int),
+        ("H", ctypes.c_int),
+        ("N", ctypes.c_int),
+        ("d", ctypes.c_int),
+        ("scale", ctypes.c_float),
+        ("tile_q", ctypes.c_int),
+        ("tile_k", ctypes.c_int),
+        ("stream", ctypes.c_void_p),
+        ("stats_out", ctypes.c_void_p),
+        ("mask_out", ctypes.c_void_p),
+        ("lse_out", ctypes.c_void_p),
+    ]
+
+
+_FWD_ARGS = [ctypes.c_void_p] * 4 + [ctypes.c_int] * 4 + [ctypes.c_float, ctypes.c_float,
+                                                           ctypes.c_int, ctypes.c_int,
+                                                           ctypes.c_void_p, ctypes.c_void_p]
+_DENSE_ARGS = [ctypes.c_void_p] * 4 + [ctypes.c_int] * 4 + [ctypes.c_float, ctypes.c_int,
+                                                            ctypes.c_int, ctypes.c_void_p,
+                                                            ctypes.c_void_p]
+
+
+def lib():
+    """Load libdsattn.so once (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is not built; run `python -m paper_2606_16317_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        for name in ("dynsparse_attn_fwd", "dynsparse_attn_fwd_lambda", "blasst_attn_fwd"):
+            getattr(L, name).argtypes = _FWD_ARGS
+            getattr(L, name).restype = ctypes.c_int
+        L.dense_attn_fwd.argtypes = _DENSE_ARGS
+        L.dense_attn_fwd.restype = ctypes.c_int
+        L.dsattn_attn_fwd_ex.argtypes = [ctypes.POINTER(DsAttnArgs)]
+        L.dsattn_attn_fwd_ex.restype = ctypes.c_int
+        L.dsattn_lambda_from_recall.argtypes = [ctypes.c_float, ctypes.c_int]
+        L.dsattn_lambda_from_recall.restype = ctypes.c_float
+        L.dsattn_last_error.argtypes = []
+        L.dsattn_last_error.restype = ctypes.c_char_p
+        L.dsattn_version.argtypes = []
+        L.dsattn_version.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def last_error() -> str:
+    return lib().dsattn_last_error().decode()
+
+
+def dsattn_lambda_from_recall(recall_target: float, N: int) -> float:
+    return float(lib().dsattn_lambda_from_recall(recall_target, N))
+
+
+def _check(rc: int, name: str):
+    if rc != 0:
+        raise RuntimeError(f"{name} failed ({rc}): {last_error()}")
+
+
+def _shape(q, k, v, o):
+    import torch
+
+    for name, t in (("q", q), ("k", k), ("v", v), ("o", o)):
+        if not isinstance(t, torch.Tensor):
+            raise TypeError(f"{name} must be a torch.Tensor")
+        if t.dtype != torch.bfloat16:
+            raise TypeError(f"{name} must be bfloat16 (got {t.dtype})")
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be on the GPU")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+        if t.dim() != 4:
+            raise ValueError(f"{name} must have shape [B, H, N, d]")
+    if not (q.shape == k.shape == v.shape == o.shape):
+        raise ValueError("q, k, v and o must have the same shape")
+    return tuple(int(x) for x in q.shape)
+
+
+def _ptr(t, numel=None, dtype=None, name="buffer"):
+    if t is None:
+        return None
+    if dtype is not None and t.dtype not in dtype:
+        raise TypeError(f"{name} has dtype {t.dtype}")
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous GPU tensor")
+    if numel is not None and t.numel() < numel:
+        raise ValueError(f"{name} needs at least {numel} elements (got {t.numel()})")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    import torch
+
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _out(q, o):
+    import torch
+
+    return torch.empty_like(q) if o is None else o
+
+
+def _buffers(B, H, N, stats_out, mask_out=None, lse_out=None):
+    import torch
+
+    n_qt = -(-N // TILE_Q)
+    n_kt = -(-N // TILE_K)
+    return (_ptr(stats_out, B * H * 4, (torch.int64, torch.uint64), "stats_out"),
+            _ptr(mask_out, B * H * n_qt * n_kt, (torch.uint8,), "mask_out"),
+            _ptr(lse_out, B * H * N, (torch.float32,), "lse_out"))
+
+
+def dynsparse_attn_fwd(q, k, v, o=None, scale=None, recall_target=0.95, tile_q=TILE_Q,
+                       tile_k=TILE_K, stats_out=None, stream=None):
+    """DynSparse forward with lambda = ln((1 - recall_target) / N); returns o."""
+    o = _out(q, o)
+    B, H, N, d = _shape(q, k, v, o)
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    st, _, _ = _buffers(B, H, N, stats_out)
+    rc = lib().dynsparse_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                  B, H, N, d, scale, recall_target, tile_q, tile_k,
+                                  _stream(stream), st)
+    _check(rc, "dynsparse_attn_fwd")
+    return o
+
+
+def dynsparse_attn_fwd_lambda(q, k, v, o=None, scale=None, lam=-6.0, tile_q=TILE_Q,
+                              tile_k=TILE_K, stats_out=None, stream=None):
+    """DynSparse forward with an explicit threshold lambda (natural log); returns o."""
+    o = _out(q, o)
+    B, H, N, d = _shape(q, k, v, o)
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    st, _, _ = _buffers(B, H, N, stats_out)
+    rc = lib().dynsparse_attn_fwd_lambda(q.data_ptr(), k.data_ptr(), v.data_ptr(),
+                                         o.data_ptr(), B, H, N, d, scale, lam, tile_q, tile_k,
+                                         _stream(stream), st)
+    _check(rc, "dynsparse_attn_fwd_lambda")
+    return o
+
+
+def blasst_attn_fwd(q, k, v, o=None, scale=None, threshold=1e-3, tile_q=TILE_Q,
+                    tile_k=TILE_K, stats_out=None, stream=None):
+    """BLASST-style forward (skip when tile max - running max < ln threshold); returns o."""
+    o = _out(q, o)
+    B, H, N, d = _shape(q, k, v, o)
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    st, _, _ = _buffers(B, H, N, stats_out)
+    rc = lib().blasst_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                               B, H, N, d, scale, threshold, tile_q, tile_k, _stream(stream),
+                               st)
+    _check(rc, "blasst_attn_fwd")
+    return o
+
+
+def dense_attn_fwd(q, k, v, o=None, scale=None, tile_q=TILE_Q, tile_k=TILE_K,
+                   stats_out=None, stream=None):
+    """Dense forward of the same kernel family; returns o."""
+    o = _out(q, o)
+    B, H, N, d = _shape(q, k, v, o)
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    st, _, _ = _buffers(B, H, N, stats_out)
+    rc = lib().dense_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                              B, H, N, d, scale, tile_q, tile_k, _stream(stream), st)
+    _check(rc, "dense_attn_fwd")
+    return o
+
+
+def dsattn_attn_fwd_ex(rule, param, q, k, v, o=None, scale=None, tile_q=TILE_Q,
+                       tile_k=TILE_K, stats_out=None, mask_out=None, lse_out=None,
+                       stream=None):
+    """Any rule (RULE_* constants) with optional stats, skip mask and LSE outputs."""
+    o = _out(q, o)
+    B, H, N, d = _shape(q, k, v, o)
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    st, mk, ls = _buffers(B, H, N, stats_out, mask_out, lse_out)
+    a = DsAttnArgs(rule, param, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                   B, H, N, d, scale, tile_q, tile_k, _stream(stream), st, mk, ls)
+    _check(lib().dsattn_attn_fwd_ex(ctypes.byref(a)), "dsattn_attn_fwd_ex")
+    return o
+
+
+__all__ = [
+    "HEAD_DIM", "TILE_Q", "TILE_K", "RULE_DENSE", "RULE_BLASST", "RULE_DYNSPARSE_RECALL",
+    "RULE_DYNSPARSE_LAMBDA", "DsAttnArgs", "lib", "last_error", "dsattn_lambda_from_recall",
+    "dynsparse_attn_fwd", "dynsparse_attn_fwd_lambda", "blasst_attn_fwd", "dense_attn_fwd",
+    "dsattn_attn_fwd_ex",
+]

@@ -1,0 +1,81 @@
+"""Build libdsattn.so in-tree with hipcc for gfx950.
+
+    python -m paper_2606_16317_amd.build            # build (always recompiles)
+    python -m paper_2606_16317_amd.build --asm DIR  # also keep the gfx950 assembly in DIR
+"""
+
+from __future__ import annotations
+
+import argparse
+import os
+import shutil
+import subprocess
+import sys
+
+PKG_DIR = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG_DIR)
+CSRC = os.path.join(PKG_DIR, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+LIB_NAME = "libdsattn.so"
+LIB_PATH = os.path.join(PKG_DIR, LIB_NAME)
+ARCH = "gfx950"
+
+SOURCES = ["fa_fwd_kernel.hip", "dsattn_api.cpp"]
+
+
+def hipcc() -> str:
+    for cand in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", shutil.which("hipcc")):
+        if cand and os.path.exists(cand):
+            return cand
+    raise RuntimeError("hipcc not found (set HIPCC or install ROCm)")
+
+
+def compile_flags() -> list:
+    return [
+        f"--offload-arch={ARCH}",
+        "-O3",
+        "-std=c++17",
+        "-fPIC",
+        # packed fp32 VALU forms stay off: plain scalar fp32 code only
+        "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+        "-Wall",
+        f"-I{INCLUDE}",
+        f"-I{CSRC}",
+    ]
+
+
+def build(verbose: bool = False, asm_dir: str | None = None) -> str:
+    """Compile every source into LIB_PATH (always recompiles); return the path."""
+    cc = hipcc()
+    tmp = LIB_PATH + ".tmp"
+    cmd = [cc, *compile_flags(), "-shared", "-o", tmp]
+    for src in SOURCES:
+        path = os.path.join(CSRC, src)
+        if src.endswith(".cpp"):
+            cmd += ["-x", "hip", path]
+        else:
+            cmd.append(path)
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, LIB_PATH)
+    if asm_dir:
+        os.makedirs(asm_dir, exist_ok=True)
+        src = os.path.join(CSRC, "fa_fwd_kernel.hip")
+        out = os.path.join(asm_dir, "fa_fwd_kernel.s")
+        subprocess.run([cc, *compile_flags(), "--cuda-device-only", "-S", src, "-o", out],
+                       check=True)
+    return LIB_PATH
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--asm", default=None, help="also write gfx950 assembly into this dir")
+    ap.add_argument("-v", "--verbose", action="store_true")
+    args = ap.parse_args(argv)
+    path = build(verbose=args.verbose, asm_dir=args.asm)
+    print(path)
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,36 @@
+// Internal interface between the C-ABI entry points and the gfx950 kernels.
+#ifndef DSATTN_FA_FWD_LAUNCH_H
+#define DSATTN_FA_FWD_LAUNCH_H
+
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+namespace dsattn {
+
+enum { kRuleDense = 0, kRuleBlasst = 1, kRuleDynSparse = 2 };
+
+struct FwdParams {
+  const uint16_t* q;   // bf16 [BH][N][128]
+  const uint16_t* k;
+  const uint16_t* v;
+  uint16_t* o;
+  int N;
+  int n_qt;            // ceil(N / 128)
+  int n_kt;            // ceil(N / 64)
+  float c;             // scale * log2(e): logits are handled in log2 units
+  float thr;           // skip threshold in log2 units (lambda*log2(e) or log2(tau))
+  uint64_t* stats;     // [BH][4] or null (zeroed beforehand)
+  uint8_t* mask;       // [BH][n_qt][n_kt] or null
+  float* lse;          // [BH][N] or null
+};
+
+// Enqueue one forward pass over `bh` heads on `stream`.
+hipError_t launch_fa_fwd(int rule, const FwdParams& p, int bh, hipStream_t stream);
+
+// Enqueue a fill of n uint64 zeros (a kernel rather than a memset node, so the call can be
+// captured into a graph and replayed).
+hipError_t launch_zero_u64(uint64_t* ptr, int n, hipStream_t stream);
+
+}  // namespace dsattn
+
+#endif
