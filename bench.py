@@ -43,8 +43,8 @@ def parse():
                     help="approximate CPU budget of the oracle baseline (0 = skip)")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense timing (profiling)")
     ap.add_argument("--sweep", action="store_true", help="one line per rule/threshold")
-    ap.add_argument("--traffic", default=None,
-                    help="JSON file with measured HBM bytes per launch of the main kernel")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="also run a plain 1 GiB -> 1 GiB copy kernel (HBM counter calibration)")
     return ap.parse_args()
 
 
@@ -78,6 +78,26 @@ def algorithmic_flops(stats, d=D):
     elems = int(stats[:, 2].sum())
     skipped = int(stats[:, 3].sum())
     return 2 * d * elems + 2 * d * (elems - skipped)
+
+
+def kernel_source_digest():
+    """sha256 of the kernel source: HBM counters are only valid for the code they measured."""
+    import hashlib
+
+    src = os.path.join(ROOT, "paper_2606_16317_amd", "csrc", "fa_fwd_kernel.hip")
+    return hashlib.sha256(open(src, "rb").read()).hexdigest()
+
+
+def measured_traffic(workload):
+    """HBM bytes per launch of the DynSparse kernel from the committed rocprofv3 counter
+    summary, or None when there is none or the kernel source changed since."""
+    path = os.path.join(ROOT, "profiles", f"hbm_traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("kernel_sha256") != kernel_source_digest():
+        return None
+    return rec.get("bytes_per_launch")
 
 
 def cpu_baseline(q, k, v, scale, lam, budget_s):
@@ -163,9 +183,13 @@ def main():
         rel_l2 = float(diff / od.float().pow(2).sum().sqrt())
 
     achieved = flop_alg / (ms * 1e-3) / 1e12
-    traffic = None
-    if args.traffic and os.path.exists(args.traffic):
-        traffic = json.load(open(args.traffic)).get("bytes_per_launch")
+    traffic = measured_traffic(w.name)
+    if args.calib_copy:
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
     cpu = None
     if args.cpu_seconds > 0:
         print("[bench] cpu oracle baseline", file=sys.stderr, flush=True)

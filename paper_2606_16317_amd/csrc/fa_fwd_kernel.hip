@@ -1,32 +1,41 @@
 // Tile-filtered FlashAttention forward kernels for gfx950 (CDNA4).
 //
 // One workgroup computes one (b, h, query tile of 128 rows); its four waves own 32 query
-// rows each.  The loop visits key tiles of 64 keys in ascending order (Section 1,
-// tile-based attention), and for every tile:
+// rows each.  Key tiles of 64 keys are visited in ascending order (Section 1, tile-based
+// attention).  For every tile the kernel
 //
-//   1. S^T = K_j Q_i^T on MFMA (bf16 inputs, fp32 accumulation) -- always computed;
-//   2. per-row tile maximum m_hat (always);
-//   3. the rule's decision (Section 3.1, Eq. 5 for DynSparse; the running-max test for
-//      BLASST), reduced over all valid rows of the 128-row tile;
-//   4. only for kept tiles: online-softmax update of the running max m and row sum l,
-//      P = exp(S - m), O = alpha O + P V_j on MFMA.
+//   1. computes S^T = K_j Q_i^T on MFMA (bf16 inputs, fp32 accumulation) -- always;
+//   2. takes the per-row tile maximum m_hat -- always;
+//   3. decides, for all valid rows of the 128-row tile together, whether the tile is
+//      kept: DynSparse (Section 3.1, Eq. 5) compares m_hat - LSE^(j-1) with lambda,
+//      BLASST compares m_hat - m^(j-1) with ln(tau), dense keeps everything;
+//   4. only for kept tiles: updates the online-softmax state (running reference max,
+//      row sum), forms P = exp(S - m) and accumulates O += P V_j on MFMA.
 //
 // Register layout (lane l of a wave, r = l % 32, g = l / 32):
-//   * the MFMA 32x32x16 output places column (l % 32) in lane l, so computing S^T = K Q^T
-//     puts one query row per lane pair (l, l ^ 32): row statistics need a single
-//     cross-half exchange instead of a 32-lane reduction;
-//   * the same lane owns P^T[., row], which is exactly what the B operand of
-//     O^T = V^T P^T needs, so P never leaves registers;
-//   * O^T accumulates in the output layout with one query row per lane, so the rescale
-//     by alpha is a per-lane scalar multiply.
+//   * the 32x32x16 MFMA puts output column (l % 32) in lane l, so S^T = K Q^T leaves one
+//     query row per lane pair (l, l ^ 32): row statistics need one cross-half exchange;
+//   * that lane pair also owns P^T[., row], which is exactly the B operand of
+//     O^T = V^T P^T, so P never leaves registers;
+//   * O^T accumulates with one query row per lane, so rescaling is a per-lane multiply.
 // The PV contraction runs over key "slots": slot i of lane half g in PV step s is the
-// key whose S^T value sits in register 8*(s%2) + i of block s/2.  V is transposed into
-// LDS in that slot order, so each V^T operand is one 16-byte LDS read.
+// key whose S^T value sits in register 8*(s%2) + i of block s/2, i.e. key
+// 32*(s/2) + 8*(2*(s%2) + i/4) + 4*g + i%4.  Slots 4c..4c+3 are four consecutive keys,
+// which is what one ds_read_b64_tr_b16 delivers from a row-major V tile.
 //
-// LDS (double buffered, 64 KiB per workgroup): K tile [64 keys][128 d] with 16-byte
-// chunks XOR-swizzled by (key % 16); V^T tile [128 d][64 slots] with 16-byte chunks
-// XOR-swizzled by ((d / 2) % 8).  Both swizzles make the 16-lane phases of the
-// ds_read_b128 operand fetches hit 16 distinct bank quads.
+// Pipeline (one barrier per key tile): S_{j+1} is computed during iteration j, so the
+// decision for tile j+1 is voted before the barrier that closes iteration j and read
+// right after it.  K is prefetched two tiles ahead and V one tile ahead, straight from
+// global memory into LDS (buffer loads with the LDS bit; rows past the sequence end come
+// back as zeros from the buffer range check).
+//
+// Online softmax uses a lazily updated reference max m_ref: O and l are rescaled only
+// when a kept tile's max exceeds m_ref by more than 8 (log2 units), so P <= 2^8.  The
+// row LSE = m_ref + log2(l) is exact either way, which is all the DynSparse rule reads.
+//
+// LDS (64 KiB per workgroup): K[2][64][128] and V[2][64][128] bf16, row-major, with
+// 16-byte chunks XOR-swizzled per row (K by key % 16, V by 2 * (key % 8)) so that the
+// MFMA operand reads of every 16-lane group touch distinct banks.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -37,87 +46,289 @@ namespace dsattn {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kD = 128;        // head dimension
 constexpr int kTQ = 128;       // query rows per workgroup (decision granularity)
 constexpr int kTK = 64;        // keys per tile
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
+constexpr int kTileElems = kTK * kD;         // 8192 bf16 = 16 KiB
+constexpr float kRescaleSlack = 8.0f;        // log2 units
 
 struct Smem {
-  alignas(16) uint16_t k[2][kTK * kD];
-  alignas(16) uint16_t vt[2][kD * kTK];
-  int vote[kWaves];
+  alignas(16) uint16_t k[2][kTileElems];
+  alignas(16) uint16_t v[2][kTileElems];
+  int vote[2][kWaves];
 };
+
+typedef __attribute__((address_space(3))) void lds_void;
 
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float log2_fast(float x) { return __builtin_amdgcn_logf(x); }
 
-// Position of tile-local key `key` (0..63) in the V^T slot order.
-__device__ __forceinline__ int slot_of_key(int key) {
-  const int b = key >> 5;           // 32-key S^T block
-  const int m = (key >> 3) & 3;     // register group (v / 4) inside the block
-  const int gg = (key >> 2) & 1;    // lane half holding the key
-  const int i4 = key & 3;
-  const int s = 2 * b + (m >> 1);   // PV step
-  const int i = ((m & 1) << 2) | i4;
-  return 16 * s + 8 * gg + i;
+// Combine a per-lane value with the one held by lane ^ 32 (the other half of the same
+// query row) using v_permlane32_swap: no LDS round trip.
+__device__ __forceinline__ float half_max(float x) {
+  const uint32_t b = __builtin_bit_cast(uint32_t, x);
+  const auto sw = __builtin_amdgcn_permlane32_swap(b, b, false, false);
+  return fmaxf(__builtin_bit_cast(float, (uint32_t)sw[0]), __builtin_bit_cast(float, (uint32_t)sw[1]));
+}
+__device__ __forceinline__ float half_sum(float x) {
+  const uint32_t b = __builtin_bit_cast(uint32_t, x);
+  const auto sw = __builtin_amdgcn_permlane32_swap(b, b, false, false);
+  return __builtin_bit_cast(float, (uint32_t)sw[0]) + __builtin_bit_cast(float, (uint32_t)sw[1]);
 }
 
-__device__ __forceinline__ int k_lds_index(int key, int chunk) {
-  return key * kD + ((chunk ^ (key & 15)) << 3);
+__device__ __forceinline__ int k_swz(int key) { return key & 15; }
+__device__ __forceinline__ int v_swz(int key) { return (key & 3) << 2; }
+
+// Element offset of (key, 16-byte chunk) inside a swizzled tile.
+__device__ __forceinline__ int k_off(int key, int chunk) {
+  return key * kD + ((chunk ^ k_swz(key)) << 3);
+}
+__device__ __forceinline__ int v_off(int key, int chunk) {
+  return key * kD + ((chunk ^ v_swz(key)) << 3);
 }
 
-__device__ __forceinline__ int vt_lds_index(int d, int slot) {
-  return d * kTK + ((((slot >> 3) ^ ((d >> 1) & 7))) << 3) + (slot & 7);
-}
-
-__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 x) {
-  return __builtin_bit_cast(bf16x8, x);
-}
-
-// Global -> register prefetch of one K/V tile (zero-filled past the sequence end).
-struct TileRegs {
-  u32x4 k[4];
-  u32x4 v[4];
-};
-
-__device__ __forceinline__ void load_tile(TileRegs& t, const uint16_t* __restrict__ kb,
-                                          const uint16_t* __restrict__ vb, int key0, int N,
-                                          int tid) {
+// Copy the 64 x 128 tile starting at key `key0` of one head into a swizzled LDS tile.
+// Wave w writes four 1 KiB blocks (4 key rows each, block u*4 + w); lane l of a block
+// lands in chunk slot l % 16 of row l / 16 and fetches the global chunk that the swizzle
+// maps there.  Keys >= N read as zero (buffer range check, one descriptor per block).
+//
+// The loads are issued from inline assembly on purpose: the compiler cannot tell which
+// LDS tile a buffer-to-LDS load writes, so it would otherwise wait for every such load
+// before the next LDS read of any tile.  The loop's own barrier waits for them instead.
+// M0 (the LDS base of the transfer) is saved and restored inside the statement.
+template <bool kIsV>
+__device__ __forceinline__ void load_tile_lds(uint16_t* tile, const uint16_t* head, int key0,
+                                              int N, int w, int lane) {
+  const int row = lane >> 4;
+  const int key_in_blk = 4 * w + row;                 // same for every block u
+  const int chunk = (lane & 15) ^ (kIsV ? v_swz(key_in_blk) : k_swz(key_in_blk));
+  const uint32_t voff = (uint32_t)(row * (kD * 2) + chunk * 16);
+  __amdgpu_buffer_rsrc_t rs[4];
+  uint32_t m0[4];
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
-    const int ci = tid + kThreads * u;
-    // K: 16 lanes cover one key row (256 contiguous bytes).
-    const int kkey = ci >> 4, kc = ci & 15;
-    const int kg = key0 + kkey;
-    t.k[u] = (kg < N) ? *reinterpret_cast<const u32x4*>(kb + (size_t)kg * kD + kc * 8)
-                      : u32x4{0, 0, 0, 0};
-    // V: a wave covers 64 keys of one 8-wide d chunk (the LDS writes then stay in one
-    // V^T row per instruction).
-    const int vkey = ci & 63, vc = ci >> 6;
-    const int vg = key0 + vkey;
-    t.v[u] = (vg < N) ? *reinterpret_cast<const u32x4*>(vb + (size_t)vg * kD + vc * 8)
-                      : u32x4{0, 0, 0, 0};
+    const int first = key0 + 16 * u + 4 * w;          // first key of block u*4 + w
+    const int remaining = N - first;
+    const int bytes = remaining > 0 ? remaining * (kD * 2) : 0;
+    rs[u] = __builtin_amdgcn_make_buffer_rsrc((void*)(head + (size_t)first * kD), (short)0, bytes,
+                                              0x00020000);
+    m0[u] = __builtin_amdgcn_readfirstlane(
+        (uint32_t)(uintptr_t)(tile + (u * kWaves + w) * 512));
+  }
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %[sv], m0\n\t"
+      "s_mov_b32 m0, %[m0a]\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %[vo], %[r0], 0 offen lds\n\t"
+      "s_mov_b32 m0, %[m0b]\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %[vo], %[r1], 0 offen lds\n\t"
+      "s_mov_b32 m0, %[m0c]\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %[vo], %[r2], 0 offen lds\n\t"
+      "s_mov_b32 m0, %[m0d]\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %[vo], %[r3], 0 offen lds\n\t"
+      "s_mov_b32 m0, %[sv]"
+      : [sv] "=&s"(saved)
+      : [m0a] "s"(m0[0]), [m0b] "s"(m0[1]), [m0c] "s"(m0[2]), [m0d] "s"(m0[3]),
+        [vo] "v"(voff), [r0] "s"(rs[0]), [r1] "s"(rs[1]), [r2] "s"(rs[2]), [r3] "s"(rs[3])
+      : "memory");
+}
+
+__device__ __forceinline__ bf16x8 lds_b128(const uint16_t* p) {
+  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p));
+}
+
+__device__ __forceinline__ bf16x4 lds_tr_b64(const uint16_t* p) {
+  typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+  const i16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p));
+  return __builtin_bit_cast(bf16x4, x);
+}
+
+// S^T (two 32-key blocks) = K_tile Q^T for this wave's 32 query rows.
+__device__ __forceinline__ void qk_tile(f32x16 (&st)[2], const uint16_t* kt, const bf16x8 (&qf)[8],
+                                        int r, int g) {
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    const int key = 32 * b + r;
+    f32x16 acc = {};
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(kt + k_off(key, 2 * s + g)), qf[s],
+                                                    acc, 0, 0, 0);
+    st[b] = acc;
   }
 }
 
-__device__ __forceinline__ void store_tile(const TileRegs& t, uint16_t* __restrict__ ks,
-                                           uint16_t* __restrict__ vts, int tid) {
+// Keys past the sequence end take no part in max or sum.
+__device__ __forceinline__ void mask_tail(f32x16 (&st)[2], int key0, int N, int g) {
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int ci = tid + kThreads * u;
-    const int kkey = ci >> 4, kc = ci & 15;
-    *reinterpret_cast<u32x4*>(ks + k_lds_index(kkey, kc)) = t.k[u];
-    const int vkey = ci & 63, vc = ci >> 6;
-    const int slot = slot_of_key(vkey);
+  for (int b = 0; b < 2; ++b)
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const uint32_t w = t.v[u][e >> 1];
-      vts[vt_lds_index(vc * 8 + e, slot)] = (uint16_t)((e & 1) ? (w >> 16) : (w & 0xFFFF));
+    for (int v = 0; v < 16; ++v) {
+      const int key = key0 + 32 * b + (v >> 2) * 8 + g * 4 + (v & 3);
+      if (key >= N) st[b][v] = -__builtin_inff();
     }
+}
+
+__device__ __forceinline__ float row_max(const f32x16 (&st)[2]) {
+  float mx = st[0][0];
+#pragma unroll
+  for (int v = 1; v < 16; ++v) mx = fmaxf(mx, st[0][v]);
+#pragma unroll
+  for (int v = 0; v < 16; ++v) mx = fmaxf(mx, st[1][v]);
+  return half_max(mx);
+}
+
+// V^T operand of PV step s for output block db: two transposed 8-byte reads.
+__device__ __forceinline__ bf16x8 v_operand(const uint16_t* vt, int db, int s, int lane) {
+  const int grp = lane >> 4;                 // 16-lane group
+  const int lg = lane & 15;
+  const int g = grp >> 1;
+  const int d = 32 * db + 16 * (grp & 1) + 4 * (lg & 3);
+  const int chunk = d >> 3, half = (d >> 2) & 1;
+  bf16x8 out;
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    const int key = 32 * (s >> 1) + 8 * (2 * (s & 1) + c) + 4 * g + (lg >> 2);
+    const bf16x4 x = lds_tr_b64(vt + v_off(key, chunk) + 4 * half);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) out[4 * c + i] = x[i];
+  }
+  return out;
+}
+
+struct RowState {
+  float m_ref;   // reference max (log2 units) of P = exp2(S*c - m_ref)
+  float m_true;  // running max of the kept tiles (BLASST metric)
+  float l_half;  // this lane's share of the kept row sum, relative to m_ref
+};
+
+// Online-softmax update for a kept tile; returns the bf16 P fragments for PV.
+__device__ __forceinline__ void softmax_tile(RowState& rs, f32x16 (&o)[4], const f32x16 (&st)[2],
+                                             float m_hat, float c, bf16x8 (&pf)[4]) {
+  rs.m_true = fmaxf(rs.m_true, m_hat);
+  const bool need = m_hat > rs.m_ref + kRescaleSlack;
+  if (__ballot(need) != 0) {
+    const float m_new = need ? m_hat : rs.m_ref;
+    const float alpha = exp2_fast(rs.m_ref - m_new);
+    rs.l_half *= alpha;
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
+    rs.m_ref = m_new;
+  }
+  const float neg_m = -rs.m_ref;
+  float psum = 0.f;
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const float e = exp2_fast(fmaf(st[b][v], c, neg_m));
+      psum += e;
+      pf[2 * b + (v >> 3)][v & 7] = (__bf16)e;
+    }
+  rs.l_half += psum;
+}
+
+__device__ __forceinline__ void pv_tile(f32x16 (&o)[4], const uint16_t* vt, const bf16x8 (&pf)[4],
+                                        int lane) {
+
+#pragma unroll
+  for (int db = 0; db < 4; ++db)
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+      o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v_operand(vt, db, s, lane), pf[s], o[db], 0,
+                                                      0, 0);
+}
+
+template <int RULE>
+__device__ __forceinline__ bool row_keeps(const RowState& rs, float m_hat, float thr) {
+  if constexpr (RULE == kRuleDynSparse) {
+    const float l_row = half_sum(rs.l_half);
+    return !(m_hat - (rs.m_ref + log2_fast(l_row)) < thr);   // Eq. 5, log2 units
+  } else {
+    return !(m_hat - rs.m_true < thr);
+  }
+}
+
+// Per-thread constants of the key-tile loop.
+struct LoopCtx {
+  const uint16_t* kb;
+  const uint16_t* vb;
+  uint8_t* mask_row;
+  float c;
+  float thr;
+  int N, n_kt, w, lane, r, g, rows_valid;
+  bool valid, ragged;
+};
+
+struct SkipCount {
+  uint32_t tiles = 0;
+  uint64_t elems = 0;
+};
+
+// One key tile j.  On entry s_cur holds S_j, mhat its row max (log2 units) and keep the
+// workgroup's decision for tile j.  On exit s_next holds S_{j+1}, mhat / keep refer to
+// tile j+1, and every wave has passed the barrier that publishes the K_{j+2} / V_{j+1}
+// buffers and the tile-(j+1) votes.
+template <int RULE>
+__device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f32x16 (&s_next)[2],
+                                              float& mhat, bool& keep, RowState& rs,
+                                              f32x16 (&o)[4], const bf16x8 (&qf)[8], Smem& sm,
+                                              const LoopCtx& cx, SkipCount& sk) {
+  const int nb = (j + 1) & 1;
+  const bool has_next = (j + 1) < cx.n_kt;
+  const bool k_ahead = (j + 2) < cx.n_kt;
+  if (has_next) load_tile_lds<true>(sm.v[nb], cx.vb, (j + 1) * kTK, cx.N, cx.w, cx.lane);
+  if (k_ahead) load_tile_lds<false>(sm.k[j & 1], cx.kb, (j + 2) * kTK, cx.N, cx.w, cx.lane);
+
+  if (cx.mask_row != nullptr && cx.w == 0 && cx.lane == 0) cx.mask_row[j] = keep ? 0 : 1;
+
+  // S_{j+1} is computed unconditionally so that it shares a basic block with the
+  // softmax of tile j (on the last tile it reads a stale buffer and is dropped).
+  if (keep) {
+    bf16x8 pf[4];
+    softmax_tile(rs, o, s_cur, mhat, cx.c, pf);
+    __builtin_amdgcn_s_setprio(1);
+    qk_tile(s_next, sm.k[nb], qf, cx.r, cx.g);
+    pv_tile(o, sm.v[j & 1], pf, cx.lane);
+    __builtin_amdgcn_s_setprio(0);
+  } else {
+    sk.tiles += 1;
+    sk.elems += (uint64_t)cx.rows_valid * (uint64_t)min(kTK, cx.N - j * kTK);
+    qk_tile(s_next, sm.k[nb], qf, cx.r, cx.g);
+  }
+
+  float mhat_next = 0.f;
+  if (has_next) {
+    if (cx.ragged && j + 2 == cx.n_kt) mask_tail(s_next, (j + 1) * kTK, cx.N, cx.g);
+    mhat_next = row_max(s_next) * cx.c;
+    if constexpr (RULE != kRuleDense) {
+      const bool wave_keeps = __ballot(cx.valid & row_keeps<RULE>(rs, mhat_next, cx.thr)) != 0;
+      if (cx.lane == 0) sm.vote[nb][cx.w] = wave_keeps ? 1 : 0;
+    }
+  }
+  // Publish this wave's LDS traffic and its V_{j+1} / K_{j+2} tile loads (both are read
+  // in the next iteration), then meet the other waves.
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  if (has_next) {
+    if constexpr (RULE != kRuleDense) {
+      const int* vt = sm.vote[nb];
+      keep = __builtin_amdgcn_readfirstlane(vt[0] | vt[1] | vt[2] | vt[3]) != 0;
+    }
+    mhat = mhat_next;
   }
 }
 
@@ -128,180 +339,91 @@ fa_fwd_kernel(FwdParams p) {
   __shared__ __attribute__((aligned(16))) Smem sm;
 
   const int tid = threadIdx.x;
-  const int w = tid >> 6;
-  const int lane = tid & 63;
-  const int r = lane & 31;
-  const int g = lane >> 5;
   const int qt = blockIdx.x;
   const int bh = blockIdx.y;
   const int N = p.N;
-  const int n_kt = p.n_kt;
-
   const size_t head_off = (size_t)bh * (size_t)N * kD;
-  const uint16_t* __restrict__ qb = p.q + head_off;
-  const uint16_t* __restrict__ kb = p.k + head_off;
-  const uint16_t* __restrict__ vb = p.v + head_off;
 
+  LoopCtx cx;
+  cx.kb = p.k + head_off;
+  cx.vb = p.v + head_off;
+  cx.mask_row = p.mask != nullptr ? p.mask + ((size_t)bh * p.n_qt + qt) * p.n_kt : nullptr;
+  cx.c = p.c;
+  cx.thr = p.thr;
+  cx.N = N;
+  cx.n_kt = p.n_kt;
+  cx.w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index, kept in an SGPR
+  cx.lane = tid & 63;
+  cx.r = cx.lane & 31;
+  cx.g = cx.lane >> 5;
   const int q0 = qt * kTQ;
-  const int qrow = q0 + w * 32 + r;
-  const bool valid = qrow < N;
-  const int rows_valid = min(kTQ, N - q0);
+  const int qrow = q0 + cx.w * 32 + cx.r;
+  cx.valid = qrow < N;
+  cx.rows_valid = min(kTQ, N - q0);
+  cx.ragged = (N % kTK) != 0;
+
+  // Stage K_0 and V_0, then K_1 (issued last so that it may stay in flight).
+  load_tile_lds<false>(sm.k[0], cx.kb, 0, N, cx.w, cx.lane);
+  load_tile_lds<true>(sm.v[0], cx.vb, 0, N, cx.w, cx.lane);
 
   // Q^T B-operand fragments: d = 16 s + 8 g + (0..7) of this lane's query row.
+  const uint16_t* qb = p.q + head_off;
   bf16x8 qf[8];
 #pragma unroll
   for (int s = 0; s < 8; ++s) {
-    u32x4 x = valid ? *reinterpret_cast<const u32x4*>(qb + (size_t)qrow * kD + 16 * s + 8 * g)
-                    : u32x4{0, 0, 0, 0};
-    qf[s] = as_bf16x8(x);
+    u32x4 x = cx.valid
+                  ? *reinterpret_cast<const u32x4*>(qb + (size_t)qrow * kD + 16 * s + 8 * cx.g)
+                  : u32x4{0, 0, 0, 0};
+    qf[s] = __builtin_bit_cast(bf16x8, x);
   }
-
   f32x16 o[4];
 #pragma unroll
   for (int db = 0; db < 4; ++db) o[db] = f32x16{};
-  float m_run = -__builtin_inff();   // running max of kept tiles, log2 units
-  float l_half = 0.f;                // this lane's share of the kept row sum
+  RowState rs{-__builtin_inff(), -__builtin_inff(), 0.f};
 
-  uint64_t tiles_skipped = 0, elems_skipped = 0;
-
-  TileRegs tr;
-  load_tile(tr, kb, vb, 0, N, tid);
-  store_tile(tr, sm.k[0], sm.vt[0], tid);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  if (cx.n_kt > 1) load_tile_lds<false>(sm.k[1], cx.kb, kTK, N, cx.w, cx.lane);
   __syncthreads();
 
-  const float c = p.c;
-  for (int j = 0; j < n_kt; ++j) {
-    const int buf = j & 1;
-    const int key0 = j * kTK;
-    const bool has_next = (j + 1) < n_kt;
-    if (has_next) load_tile(tr, kb, vb, key0 + kTK, N, tid);
+  f32x16 sa[2], sb[2];
+  qk_tile(sa, sm.k[0], qf, cx.r, cx.g);
+  if (cx.ragged && cx.n_kt == 1) mask_tail(sa, 0, N, cx.g);
+  float mhat = row_max(sa) * cx.c;
+  bool keep = true;                          // the first tile is always kept
+  SkipCount sk;
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();                           // K_0 consumed before K_2 lands there
 
-    // ---- S^T = K_j Q^T: two 32-key blocks, eight 16-wide d steps each --------------
-    f32x16 st[2];
-#pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      st[b] = f32x16{};
-      const int key = 32 * b + r;
-#pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        const bf16x8 a = as_bf16x8(
-            *reinterpret_cast<const u32x4*>(sm.k[buf] + k_lds_index(key, 2 * s + g)));
-        st[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[s], st[b], 0, 0, 0);
-      }
-    }
-    // Keys past the end of the sequence take no part in max or sum.
-    if (key0 + kTK > N) {
-#pragma unroll
-      for (int b = 0; b < 2; ++b)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int key = key0 + 32 * b + (v >> 2) * 8 + g * 4 + (v & 3);
-          if (key >= N) st[b][v] = -__builtin_inff();
-        }
-    }
-
-    // ---- tile row max (raw logits; c > 0 so scaling commutes with max) ------------
-    float mx = st[0][0];
-#pragma unroll
-    for (int v = 1; v < 16; ++v) mx = fmaxf(mx, st[0][v]);
-#pragma unroll
-    for (int v = 0; v < 16; ++v) mx = fmaxf(mx, st[1][v]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_hat = mx * c;
-
-    // ---- decision --------------------------------------------------------------
-    bool keep = true;
-    if constexpr (RULE != kRuleDense) {
-      float t;
-      if constexpr (RULE == kRuleDynSparse) {
-        const float l_row = l_half + __shfl_xor(l_half, 32);
-        t = m_hat - (m_run + log2_fast(l_row));   // Eq. 5 in log2 units
-      } else {
-        t = m_hat - m_run;
-      }
-      const bool row_keeps = valid && !(t < p.thr);
-      const bool wave_keeps = __ballot(row_keeps) != 0;
-      if (lane == 0) sm.vote[w] = wave_keeps ? 1 : 0;
-      __syncthreads();
-      keep = (sm.vote[0] | sm.vote[1] | sm.vote[2] | sm.vote[3]) != 0;
-      if (!keep) {
-        tiles_skipped += 1;
-        elems_skipped += (uint64_t)rows_valid * (uint64_t)min(kTK, N - key0);
-      }
-      if (p.mask != nullptr && tid == 0)
-        p.mask[((size_t)bh * p.n_qt + qt) * n_kt + j] = keep ? 0 : 1;
-    } else {
-      if (p.mask != nullptr && tid == 0) p.mask[((size_t)bh * p.n_qt + qt) * n_kt + j] = 0;
-    }
-
-    if (keep) {
-      // ---- online softmax (Eq. 6 state) --------------------------------------
-      const float m_new = fmaxf(m_run, m_hat);
-      const float alpha = exp2_fast(m_run - m_new);
-      const float neg_m = -m_new;
-      float psum = 0.f;
-      bf16x8 pf[4];
-#pragma unroll
-      for (int b = 0; b < 2; ++b)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const float e = exp2_fast(fmaf(st[b][v], c, neg_m));
-          psum += e;
-          pf[2 * b + (v >> 3)][v & 7] = (__bf16)e;
-        }
-      l_half = fmaf(alpha, l_half, psum);
-#pragma unroll
-      for (int db = 0; db < 4; ++db)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
-      m_run = m_new;
-
-      // ---- O^T += V^T P^T ------------------------------------------------------
-#pragma unroll
-      for (int db = 0; db < 4; ++db) {
-        const int d = 32 * db + r;
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-          const bf16x8 a = as_bf16x8(*reinterpret_cast<const u32x4*>(
-              sm.vt[buf] + vt_lds_index(d, 16 * s + 8 * g)));
-          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[s], o[db], 0, 0, 0);
-        }
-      }
-    }
-
-    if (has_next) store_tile(tr, sm.k[buf ^ 1], sm.vt[buf ^ 1], tid);
-    __syncthreads();
+  // Unrolled by two so that S_j / S_{j+1} alternate between sa and sb without copies.
+  for (int j = 0; j < cx.n_kt; j += 2) {
+    key_tile_step<RULE>(j, sa, sb, mhat, keep, rs, o, qf, sm, cx, sk);
+    if (j + 1 < cx.n_kt) key_tile_step<RULE>(j + 1, sb, sa, mhat, keep, rs, o, qf, sm, cx, sk);
   }
 
   // ---- epilogue: renormalise over kept keys, store O (bf16) and the row LSE --------
-  const float l_row = l_half + __shfl_xor(l_half, 32);
+  const float l_row = half_sum(rs.l_half);
   const float inv = 1.0f / l_row;
-  if (valid) {
-    uint16_t* __restrict__ orow = p.o + head_off + (size_t)qrow * kD;
+  if (cx.valid) {
+    uint16_t* orow = p.o + head_off + (size_t)qrow * kD;
 #pragma unroll
     for (int db = 0; db < 4; ++db)
 #pragma unroll
       for (int grp = 0; grp < 4; ++grp) {
-        __bf16 h0 = (__bf16)(o[db][4 * grp + 0] * inv);
-        __bf16 h1 = (__bf16)(o[db][4 * grp + 1] * inv);
-        __bf16 h2 = (__bf16)(o[db][4 * grp + 2] * inv);
-        __bf16 h3 = (__bf16)(o[db][4 * grp + 3] * inv);
-        const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, h0) |
-                            ((uint32_t)__builtin_bit_cast(uint16_t, h1) << 16);
-        const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, h2) |
-                            ((uint32_t)__builtin_bit_cast(uint16_t, h3) << 16);
-        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-        *reinterpret_cast<u32x2*>(orow + 32 * db + 8 * grp + 4 * g) = u32x2{lo, hi};
+        bf16x4 h;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) h[i] = (__bf16)(o[db][4 * grp + i] * inv);
+        *reinterpret_cast<u32x2*>(orow + 32 * db + 8 * grp + 4 * cx.g) =
+            __builtin_bit_cast(u32x2, h);
       }
-    if (p.lse != nullptr && g == 0)
-      p.lse[(size_t)bh * N + qrow] = (m_run + log2_fast(l_row)) * 0.69314718055994530942f;
+    if (p.lse != nullptr && cx.g == 0)
+      p.lse[(size_t)bh * N + qrow] = (rs.m_ref + log2_fast(l_row)) * 0.69314718055994530942f;
   }
   if (p.stats != nullptr && tid == 0) {
     unsigned long long* st = reinterpret_cast<unsigned long long*>(p.stats) + (size_t)bh * 4;
-    atomicAdd(st + 0, (unsigned long long)n_kt);
-    atomicAdd(st + 1, (unsigned long long)tiles_skipped);
-    atomicAdd(st + 2, (unsigned long long)rows_valid * (unsigned long long)N);
-    atomicAdd(st + 3, (unsigned long long)elems_skipped);
+    atomicAdd(st + 0, (unsigned long long)cx.n_kt);
+    atomicAdd(st + 1, (unsigned long long)sk.tiles);
+    atomicAdd(st + 2, (unsigned long long)cx.rows_valid * (unsigned long long)N);
+    atomicAdd(st + 3, (unsigned long long)sk.elems);
   }
 }
 
