@@ -9,8 +9,8 @@
 //   3. decides, for all valid rows of the 128-row tile together, whether the tile is
 //      kept: DynSparse (Section 3.1, Eq. 5) compares m_hat - LSE^(j-1) with lambda,
 //      BLASST compares m_hat - m^(j-1) with ln(tau), dense keeps everything;
-//   4. only for kept tiles: updates the online-softmax state (running reference max,
-//      row sum), forms P = exp(S - m) and accumulates O += P V_j on MFMA.
+//   4. only for kept tiles: updates the online-softmax state (reference max, row sum),
+//      forms P = exp(S - m) and accumulates O += P V_j on MFMA.
 //
 // Register layout (lane l of a wave, r = l % 32, g = l / 32):
 //   * the 32x32x16 MFMA puts output column (l % 32) in lane l, so S^T = K Q^T leaves one
@@ -27,15 +27,17 @@
 // decision for tile j+1 is voted before the barrier that closes iteration j and read
 // right after it.  K is prefetched two tiles ahead and V one tile ahead, straight from
 // global memory into LDS (buffer loads with the LDS bit; rows past the sequence end come
-// back as zeros from the buffer range check).
+// back as zeros from the buffer range check).  Inside an iteration the instruction
+// order is fixed by scheduling fences: each of the 16 S_{j+1} MFMAs carries two
+// elements of the tile-j softmax, and MFMA operands are read from LDS two MFMAs ahead.
 //
 // Online softmax uses a lazily updated reference max m_ref: O and l are rescaled only
 // when a kept tile's max exceeds m_ref by more than 8 (log2 units), so P <= 2^8.  The
 // row LSE = m_ref + log2(l) is exact either way, which is all the DynSparse rule reads.
 //
 // LDS (64 KiB per workgroup): K[2][64][128] and V[2][64][128] bf16, row-major, with
-// 16-byte chunks XOR-swizzled per row (K by key % 16, V by 2 * (key % 8)) so that the
-// MFMA operand reads of every 16-lane group touch distinct banks.
+// 16-byte chunks XOR-swizzled per row (K by key % 16, V by 4 * (key % 4)) so that the
+// MFMA operand reads of every 16- and 32-lane group touch distinct banks.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -63,13 +65,12 @@ constexpr float kRescaleSlack = 8.0f;        // log2 units
 struct Smem {
   alignas(16) uint16_t k[2][kTileElems];
   alignas(16) uint16_t v[2][kTileElems];
-  int vote[2][kWaves];
+  alignas(4) uint8_t vote[2][kWaves];        // one byte per wave, read back as one dword
 };
-
-typedef __attribute__((address_space(3))) void lds_void;
 
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float log2_fast(float x) { return __builtin_amdgcn_logf(x); }
+__device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 
 // Combine a per-lane value with the one held by lane ^ 32 (the other half of the same
 // query row) using v_permlane32_swap: no LDS round trip.
@@ -96,53 +97,52 @@ __device__ __forceinline__ int v_off(int key, int chunk) {
 }
 
 // Copy the 64 x 128 tile starting at key `key0` of one head into a swizzled LDS tile.
-// Wave w writes four 1 KiB blocks (4 key rows each, block u*4 + w); lane l of a block
-// lands in chunk slot l % 16 of row l / 16 and fetches the global chunk that the swizzle
-// maps there.  Keys >= N read as zero (buffer range check, one descriptor per block).
+// Wave w writes four 1 KiB blocks u*4 + w (4 key rows each); lane l of a block lands in
+// chunk slot l % 16 of row l / 16 and fetches the global chunk that the swizzle maps
+// there.  `rs` covers the whole head (N rows of 256 bytes), so keys >= N fail the buffer
+// range check and arrive as zeros.  `voff` is the lane's byte offset inside a block,
+// which is the same for all four blocks of every tile (the swizzles depend on the key
+// modulo 16 only).
 //
 // The loads are issued from inline assembly on purpose: the compiler cannot tell which
 // LDS tile a buffer-to-LDS load writes, so it would otherwise wait for every such load
 // before the next LDS read of any tile.  The loop's own barrier waits for them instead.
-// M0 (the LDS base of the transfer) is saved and restored inside the statement.
-template <bool kIsV>
-__device__ __forceinline__ void load_tile_lds(uint16_t* tile, const uint16_t* head, int key0,
-                                              int N, int w, int lane) {
-  const int row = lane >> 4;
-  const int key_in_blk = 4 * w + row;                 // same for every block u
-  const int chunk = (lane & 15) ^ (kIsV ? v_swz(key_in_blk) : k_swz(key_in_blk));
-  const uint32_t voff = (uint32_t)(row * (kD * 2) + chunk * 16);
-  __amdgpu_buffer_rsrc_t rs[4];
-  uint32_t m0[4];
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int first = key0 + 16 * u + 4 * w;          // first key of block u*4 + w
-    const int remaining = N - first;
-    const int bytes = remaining > 0 ? remaining * (kD * 2) : 0;
-    rs[u] = __builtin_amdgcn_make_buffer_rsrc((void*)(head + (size_t)first * kD), (short)0, bytes,
-                                              0x00020000);
-    m0[u] = __builtin_amdgcn_readfirstlane(
-        (uint32_t)(uintptr_t)(tile + (u * kWaves + w) * 512));
-  }
+// M0 (the LDS base of the transfer) is saved and restored inside the statement, with
+// the wait state an M0 write needs before an LDS-DMA instruction.
+__device__ __forceinline__ void load_tile_lds(uint16_t* tile, __amdgpu_buffer_rsrc_t rs,
+                                              uint32_t voff, int key0, int w) {
+  const uint32_t o0 = voff + (uint32_t)key0 * (kD * 2);
+  const uint32_t lds0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(tile + w * 512));
   uint32_t saved;
   asm volatile(
       "s_mov_b32 %[sv], m0\n\t"
-      "s_mov_b32 m0, %[m0a]\n\t"
+      "s_mov_b32 m0, %[l0]\n\t"
       "s_nop 0\n\t"
-      "buffer_load_dwordx4 %[vo], %[r0], 0 offen lds\n\t"
-      "s_mov_b32 m0, %[m0b]\n\t"
+      "buffer_load_dwordx4 %[o0], %[rs], 0 offen lds\n\t"
+      "s_add_u32 m0, %[l0], 0x1000\n\t"
       "s_nop 0\n\t"
-      "buffer_load_dwordx4 %[vo], %[r1], 0 offen lds\n\t"
-      "s_mov_b32 m0, %[m0c]\n\t"
+      "buffer_load_dwordx4 %[o1], %[rs], 0 offen lds\n\t"
+      "s_add_u32 m0, %[l0], 0x2000\n\t"
       "s_nop 0\n\t"
-      "buffer_load_dwordx4 %[vo], %[r2], 0 offen lds\n\t"
-      "s_mov_b32 m0, %[m0d]\n\t"
+      "buffer_load_dwordx4 %[o2], %[rs], 0 offen lds\n\t"
+      "s_add_u32 m0, %[l0], 0x3000\n\t"
       "s_nop 0\n\t"
-      "buffer_load_dwordx4 %[vo], %[r3], 0 offen lds\n\t"
+      "buffer_load_dwordx4 %[o3], %[rs], 0 offen lds\n\t"
       "s_mov_b32 m0, %[sv]"
       : [sv] "=&s"(saved)
-      : [m0a] "s"(m0[0]), [m0b] "s"(m0[1]), [m0c] "s"(m0[2]), [m0d] "s"(m0[3]),
-        [vo] "v"(voff), [r0] "s"(rs[0]), [r1] "s"(rs[1]), [r2] "s"(rs[2]), [r3] "s"(rs[3])
-      : "memory");
+      : [l0] "s"(lds0), [o0] "v"(o0), [o1] "v"(o0 + 4096u), [o2] "v"(o0 + 8192u),
+        [o3] "v"(o0 + 12288u), [rs] "s"(rs)
+      : "memory", "scc");
+}
+
+// Lane offset inside a 1 KiB block (4 key rows) for a K (swizzle key % 16) or V
+// (swizzle 4 * (key % 4)) tile.
+template <bool kIsV>
+__device__ __forceinline__ uint32_t tile_lane_offset(int w, int lane) {
+  const int row = lane >> 4;
+  const int key = 4 * w + row;              // key index modulo 16 of this lane's row
+  const int chunk = (lane & 15) ^ (kIsV ? v_swz(key) : k_swz(key));
+  return (uint32_t)(key * (kD * 2) + chunk * 16);
 }
 
 __device__ __forceinline__ bf16x8 lds_b128(const uint16_t* p) {
@@ -155,43 +155,15 @@ __device__ __forceinline__ bf16x4 lds_tr_b64(const uint16_t* p) {
   return __builtin_bit_cast(bf16x4, x);
 }
 
-// S^T (two 32-key blocks) = K_tile Q^T for this wave's 32 query rows.
-__device__ __forceinline__ void qk_tile(f32x16 (&st)[2], const uint16_t* kt, const bf16x8 (&qf)[8],
-                                        int r, int g) {
-#pragma unroll
-  for (int b = 0; b < 2; ++b) {
-    const int key = 32 * b + r;
-    f32x16 acc = {};
-#pragma unroll
-    for (int s = 0; s < 8; ++s)
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(kt + k_off(key, 2 * s + g)), qf[s],
-                                                    acc, 0, 0, 0);
-    st[b] = acc;
-  }
+// K operand of S^T MFMA number i (chains alternate: block b = i % 2, d step s = i / 2).
+__device__ __forceinline__ bf16x8 k_operand(const uint16_t* kt, int i, int r, int g) {
+  return lds_b128(kt + k_off(32 * (i & 1) + r, 2 * (i >> 1) + g));
 }
 
-// Keys past the sequence end take no part in max or sum.
-__device__ __forceinline__ void mask_tail(f32x16 (&st)[2], int key0, int N, int g) {
-#pragma unroll
-  for (int b = 0; b < 2; ++b)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int key = key0 + 32 * b + (v >> 2) * 8 + g * 4 + (v & 3);
-      if (key >= N) st[b][v] = -__builtin_inff();
-    }
-}
-
-__device__ __forceinline__ float row_max(const f32x16 (&st)[2]) {
-  float mx = st[0][0];
-#pragma unroll
-  for (int v = 1; v < 16; ++v) mx = fmaxf(mx, st[0][v]);
-#pragma unroll
-  for (int v = 0; v < 16; ++v) mx = fmaxf(mx, st[1][v]);
-  return half_max(mx);
-}
-
-// V^T operand of PV step s for output block db: two transposed 8-byte reads.
-__device__ __forceinline__ bf16x8 v_operand(const uint16_t* vt, int db, int s, int lane) {
+// V^T operand of PV MFMA number i (output block db = i % 4, key step s = i / 4): two
+// transposed 8-byte reads of four consecutive keys each.
+__device__ __forceinline__ bf16x8 v_operand(const uint16_t* vt, int i, int lane) {
+  const int db = i & 3, s = i >> 2;
   const int grp = lane >> 4;                 // 16-lane group
   const int lg = lane & 15;
   const int g = grp >> 1;
@@ -203,9 +175,30 @@ __device__ __forceinline__ bf16x8 v_operand(const uint16_t* vt, int db, int s, i
     const int key = 32 * (s >> 1) + 8 * (2 * (s & 1) + c) + 4 * g + (lg >> 2);
     const bf16x4 x = lds_tr_b64(vt + v_off(key, chunk) + 4 * half);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) out[4 * c + i] = x[i];
+    for (int t = 0; t < 4; ++t) out[4 * c + t] = x[t];
   }
   return out;
+}
+
+// Keys past the sequence end take no part in max or sum.  Register v of block b holds
+// key key0 + 4g + (32b + 8(v/4) + v%4): compare that compile-time offset with one
+// per-lane limit so no per-element index stays live.
+__device__ __forceinline__ void mask_tail(f32x16 (&st)[2], int key0, int N, int g) {
+  const int lim = N - key0 - 4 * g;
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+#pragma unroll
+    for (int v = 0; v < 16; ++v)
+      if (32 * b + (v >> 2) * 8 + (v & 3) >= lim) st[b][v] = -__builtin_inff();
+}
+
+__device__ __forceinline__ float row_max(const f32x16 (&st)[2]) {
+  float mx = st[0][0];
+#pragma unroll
+  for (int v = 1; v < 16; ++v) mx = fmaxf(mx, st[0][v]);
+#pragma unroll
+  for (int v = 0; v < 16; ++v) mx = fmaxf(mx, st[1][v]);
+  return half_max(mx);
 }
 
 struct RowState {
@@ -214,9 +207,8 @@ struct RowState {
   float l_half;  // this lane's share of the kept row sum, relative to m_ref
 };
 
-// Online-softmax update for a kept tile; returns the bf16 P fragments for PV.
-__device__ __forceinline__ void softmax_tile(RowState& rs, f32x16 (&o)[4], const f32x16 (&st)[2],
-                                             float m_hat, float c, bf16x8 (&pf)[4]) {
+// Lazy rescale at the start of a kept tile with row max m_hat (log2 units).
+__device__ __forceinline__ void rescale_if_needed(RowState& rs, f32x16 (&o)[4], float m_hat) {
   rs.m_true = fmaxf(rs.m_true, m_hat);
   const bool need = m_hat > rs.m_ref + kRescaleSlack;
   if (__ballot(need) != 0) {
@@ -229,28 +221,70 @@ __device__ __forceinline__ void softmax_tile(RowState& rs, f32x16 (&o)[4], const
       for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
     rs.m_ref = m_new;
   }
-  const float neg_m = -rs.m_ref;
-  float psum = 0.f;
-#pragma unroll
-  for (int b = 0; b < 2; ++b)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const float e = exp2_fast(fmaf(st[b][v], c, neg_m));
-      psum += e;
-      pf[2 * b + (v >> 3)][v & 7] = (__bf16)e;
-    }
-  rs.l_half += psum;
 }
 
-__device__ __forceinline__ void pv_tile(f32x16 (&o)[4], const uint16_t* vt, const bf16x8 (&pf)[4],
-                                        int lane) {
+// Softmax numerator of S^T element e (0..31, block e / 16, register e % 16).
+__device__ __forceinline__ void softmax_elem(const f32x16 (&st)[2], int e, float c, float neg_m,
+                                             float& psum, bf16x8 (&pf)[4]) {
+  const int b = e >> 4, v = e & 15;
+  const float x = exp2_fast(fmaf(st[b][v], c, neg_m));
+  psum += x;
+  pf[2 * b + (v >> 3)][v & 7] = (__bf16)x;
+}
 
+// Kept tile j: softmax of S_j interleaved with the 16 MFMAs of S_{j+1} = K_{j+1} Q^T,
+// then O += P V_j.  MFMA operands are read from LDS two MFMAs ahead.
+__device__ __forceinline__ void kept_tile(RowState& rs, f32x16 (&o)[4], const f32x16 (&s_cur)[2],
+                                          float m_hat, float c, f32x16 (&s_next)[2],
+                                          const uint16_t* kt, const uint16_t* vt,
+                                          const bf16x8 (&qf)[8], int r, int g, int lane) {
+  rescale_if_needed(rs, o, m_hat);
+  const float neg_m = -rs.m_ref;
+  float psum = 0.f;
+  bf16x8 pf[4];
+  bf16x8 ka[3], va[3];
+  ka[0] = k_operand(kt, 0, r, g);
+  ka[1] = k_operand(kt, 1, r, g);
+  sched_fence();
+  __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-  for (int db = 0; db < 4; ++db)
+  for (int i = 0; i < 16; ++i) {
+    if (i + 2 < 16)
+      ka[(i + 2) % 3] = k_operand(kt, i + 2, r, g);
+    else
+      va[i - 14] = v_operand(vt, i - 14, lane);
+    f32x16& acc = s_next[i & 1];
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[i % 3], qf[i >> 1],
+                                                  i < 2 ? f32x16{} : acc, 0, 0, 0);
+    softmax_elem(s_cur, 2 * i, c, neg_m, psum, pf);
+    softmax_elem(s_cur, 2 * i + 1, c, neg_m, psum, pf);
+    sched_fence();
+  }
+  rs.l_half += psum;
 #pragma unroll
-    for (int s = 0; s < 4; ++s)
-      o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v_operand(vt, db, s, lane), pf[s], o[db], 0,
-                                                      0, 0);
+  for (int i = 0; i < 16; ++i) {
+    if (i + 2 < 16) va[(i + 2) % 3] = v_operand(vt, i + 2, lane);
+    o[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i % 3], pf[i >> 2], o[i & 3], 0, 0, 0);
+    sched_fence();
+  }
+  __builtin_amdgcn_s_setprio(0);
+}
+
+// Skipped tile j: only S_{j+1} = K_{j+1} Q^T.
+__device__ __forceinline__ void skipped_tile(f32x16 (&s_next)[2], const uint16_t* kt,
+                                             const bf16x8 (&qf)[8], int r, int g) {
+  bf16x8 ka[3];
+  ka[0] = k_operand(kt, 0, r, g);
+  ka[1] = k_operand(kt, 1, r, g);
+  sched_fence();
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    if (i + 2 < 16) ka[(i + 2) % 3] = k_operand(kt, i + 2, r, g);
+    f32x16& acc = s_next[i & 1];
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[i % 3], qf[i >> 1],
+                                                  i < 2 ? f32x16{} : acc, 0, 0, 0);
+    sched_fence();
+  }
 }
 
 template <int RULE>
@@ -265,8 +299,9 @@ __device__ __forceinline__ bool row_keeps(const RowState& rs, float m_hat, float
 
 // Per-thread constants of the key-tile loop.
 struct LoopCtx {
-  const uint16_t* kb;
-  const uint16_t* vb;
+  __amdgpu_buffer_rsrc_t krs;   // K / V of this head as buffer resources
+  __amdgpu_buffer_rsrc_t vrs;
+  uint32_t koff, voff;          // lane offsets inside a 1 KiB tile block
   uint8_t* mask_row;
   float c;
   float thr;
@@ -290,25 +325,21 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
                                               const LoopCtx& cx, SkipCount& sk) {
   const int nb = (j + 1) & 1;
   const bool has_next = (j + 1) < cx.n_kt;
-  const bool k_ahead = (j + 2) < cx.n_kt;
-  if (has_next) load_tile_lds<true>(sm.v[nb], cx.vb, (j + 1) * kTK, cx.N, cx.w, cx.lane);
-  if (k_ahead) load_tile_lds<false>(sm.k[j & 1], cx.kb, (j + 2) * kTK, cx.N, cx.w, cx.lane);
+  // Issued unconditionally: past the last tile the range check returns zeros into
+  // buffers nobody reads, and the loop body stays free of branches here.
+  load_tile_lds(sm.v[nb], cx.vrs, cx.voff, (j + 1) * kTK, cx.w);
+  load_tile_lds(sm.k[j & 1], cx.krs, cx.koff, (j + 2) * kTK, cx.w);
 
   if (cx.mask_row != nullptr && cx.w == 0 && cx.lane == 0) cx.mask_row[j] = keep ? 0 : 1;
 
-  // S_{j+1} is computed unconditionally so that it shares a basic block with the
-  // softmax of tile j (on the last tile it reads a stale buffer and is dropped).
+  // S_{j+1} is computed on both paths (on the last tile it reads a stale buffer and is
+  // dropped).
   if (keep) {
-    bf16x8 pf[4];
-    softmax_tile(rs, o, s_cur, mhat, cx.c, pf);
-    __builtin_amdgcn_s_setprio(1);
-    qk_tile(s_next, sm.k[nb], qf, cx.r, cx.g);
-    pv_tile(o, sm.v[j & 1], pf, cx.lane);
-    __builtin_amdgcn_s_setprio(0);
+    kept_tile(rs, o, s_cur, mhat, cx.c, s_next, sm.k[nb], sm.v[j & 1], qf, cx.r, cx.g, cx.lane);
   } else {
     sk.tiles += 1;
     sk.elems += (uint64_t)cx.rows_valid * (uint64_t)min(kTK, cx.N - j * kTK);
-    qk_tile(s_next, sm.k[nb], qf, cx.r, cx.g);
+    skipped_tile(s_next, sm.k[nb], qf, cx.r, cx.g);
   }
 
   float mhat_next = 0.f;
@@ -321,13 +352,12 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
     }
   }
   // Publish this wave's LDS traffic and its V_{j+1} / K_{j+2} tile loads (both are read
-  // in the next iteration), then meet the other waves.
+  // in the next iteration), then meet the other waves.  (__syncthreads() would add a
+  // fence that makes the compiler drain every load again on its own.)
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
   if (has_next) {
-    if constexpr (RULE != kRuleDense) {
-      const int* vt = sm.vote[nb];
-      keep = __builtin_amdgcn_readfirstlane(vt[0] | vt[1] | vt[2] | vt[3]) != 0;
-    }
+    if constexpr (RULE != kRuleDense)
+      keep = __builtin_amdgcn_readfirstlane(*reinterpret_cast<const uint32_t*>(sm.vote[nb])) != 0;
     mhat = mhat_next;
   }
 }
@@ -345,8 +375,11 @@ fa_fwd_kernel(FwdParams p) {
   const size_t head_off = (size_t)bh * (size_t)N * kD;
 
   LoopCtx cx;
-  cx.kb = p.k + head_off;
-  cx.vb = p.v + head_off;
+  const int head_bytes = N * (kD * 2);
+  cx.krs = __builtin_amdgcn_make_buffer_rsrc((void*)(p.k + head_off), (short)0, head_bytes,
+                                             0x00020000);
+  cx.vrs = __builtin_amdgcn_make_buffer_rsrc((void*)(p.v + head_off), (short)0, head_bytes,
+                                             0x00020000);
   cx.mask_row = p.mask != nullptr ? p.mask + ((size_t)bh * p.n_qt + qt) * p.n_kt : nullptr;
   cx.c = p.c;
   cx.thr = p.thr;
@@ -354,6 +387,8 @@ fa_fwd_kernel(FwdParams p) {
   cx.n_kt = p.n_kt;
   cx.w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index, kept in an SGPR
   cx.lane = tid & 63;
+  cx.koff = tile_lane_offset<false>(cx.w, cx.lane);
+  cx.voff = tile_lane_offset<true>(cx.w, cx.lane);
   cx.r = cx.lane & 31;
   cx.g = cx.lane >> 5;
   const int q0 = qt * kTQ;
@@ -362,9 +397,9 @@ fa_fwd_kernel(FwdParams p) {
   cx.rows_valid = min(kTQ, N - q0);
   cx.ragged = (N % kTK) != 0;
 
-  // Stage K_0 and V_0, then K_1 (issued last so that it may stay in flight).
-  load_tile_lds<false>(sm.k[0], cx.kb, 0, N, cx.w, cx.lane);
-  load_tile_lds<true>(sm.v[0], cx.vb, 0, N, cx.w, cx.lane);
+  // Stage K_0 and V_0, then K_1.
+  load_tile_lds(sm.k[0], cx.krs, cx.koff, 0, cx.w);
+  load_tile_lds(sm.v[0], cx.vrs, cx.voff, 0, cx.w);
 
   // Q^T B-operand fragments: d = 16 s + 8 g + (0..7) of this lane's query row.
   const uint16_t* qb = p.q + head_off;
@@ -381,18 +416,16 @@ fa_fwd_kernel(FwdParams p) {
   for (int db = 0; db < 4; ++db) o[db] = f32x16{};
   RowState rs{-__builtin_inff(), -__builtin_inff(), 0.f};
 
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  if (cx.n_kt > 1) load_tile_lds<false>(sm.k[1], cx.kb, kTK, N, cx.w, cx.lane);
-  __syncthreads();
+  load_tile_lds(sm.k[1], cx.krs, cx.koff, kTK, cx.w);
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 
   f32x16 sa[2], sb[2];
-  qk_tile(sa, sm.k[0], qf, cx.r, cx.g);
+  skipped_tile(sa, sm.k[0], qf, cx.r, cx.g);   // S_0
   if (cx.ragged && cx.n_kt == 1) mask_tail(sa, 0, N, cx.g);
   float mhat = row_max(sa) * cx.c;
   bool keep = true;                          // the first tile is always kept
   SkipCount sk;
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();                           // K_0 consumed before K_2 lands there
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");  // K_0 consumed
 
   // Unrolled by two so that S_j / S_{j+1} alternate between sa and sb without copies.
   for (int j = 0; j < cx.n_kt; j += 2) {
