@@ -28,7 +28,8 @@
  *   written except stats_out, which is zeroed.
  * Memory: every pointer is a device pointer allocated by the caller on the current HIP
  *   device; the library never allocates, frees or retains memory.  q, k, v are read-only;
- *   o must not alias q, k or v.
+ *   o must not alias q, k or v; q, k, v, o must be 16-byte aligned and lse_out 4-byte
+ *   aligned.
  * Execution: asynchronous on `stream` (0 = the null stream).  Argument errors are found
  *   on the host before anything is enqueued.  Calls that share output buffers on one
  *   stream are ordered by the stream; on different streams they race.
@@ -45,6 +46,7 @@
 #ifndef DSATTN_H
 #define DSATTN_H
 
+#include <stddef.h>
 #include <stdint.h>
 #include <hip/hip_runtime_api.h>
 
@@ -124,6 +126,65 @@ typedef struct dsattn_args {
 } dsattn_args;
 
 int dsattn_attn_fwd_ex(const dsattn_args* args);
+
+/*
+ * Spatio-temporal token reordering (Section 3.2, closing remark on hyperparameter
+ * selection; Section 2 describes the same grouping of tokens that are near in time and
+ * space).  A video transformer flattens its T x Y x X latent grid row-major (x fastest),
+ * so a 128-token query tile spans whole rows of x and a key tile's neighbours in y and t
+ * lie far away in the sequence.  Regrouping the tokens into bt x by x bx blocks before the
+ * attention puts neighbours into the same tile.
+ */
+
+/*
+ * Host function.  Writes the gather map of the blocked order into perm_out (host memory,
+ * int32 [T*Y*X]): blocks are visited in row-major block order (the last block along an
+ * axis may be clipped by the grid), the tokens of a block in row-major order; position i
+ * of the reordered sequence holds original token perm_out[i] = (t*Y + y)*X + x.
+ * All extents must be positive and T*Y*X < 2^31.  Returns DSATTN_EINVAL otherwise, or
+ * when perm_out is NULL or device-only memory.
+ */
+int dsattn_block_order(int T, int Y, int X, int bt, int by, int bx, int32_t* perm_out);
+
+/*
+ * Row moves along the sequence axis of a device tensor [BH][N][row_bytes]:
+ *   dsattn_gather_rows:  dst[b][i] = src[b][index[i]]
+ *   dsattn_scatter_rows: dst[b][index[i]] = src[b][i]
+ * index is a device int32 [N] array shared by all BH heads.  An entry outside [0, N)
+ * never causes a memory access: gather writes a zero row for it, scatter drops the row.
+ * With a non-injective index, scatter writes the duplicates in an unspecified order.
+ * row_bytes must be a positive multiple of 4 and N * row_bytes <= 2^33; src, dst and
+ * index must be 4-byte aligned device pointers and src and dst must not overlap
+ * (16-byte alignment and row_bytes % 16 == 0 select the 16-byte-per-lane path).
+ * 0 <= BH <= 65535.  Asynchronous on `stream`.
+ */
+int dsattn_gather_rows(const void* src, void* dst, const int32_t* index, int BH, int N,
+                       int row_bytes, hipStream_t stream);
+int dsattn_scatter_rows(const void* src, void* dst, const int32_t* index, int BH, int N,
+                        int row_bytes, hipStream_t stream);
+
+/*
+ * Workspace, in bytes, that dsattn_attn_fwd_reordered needs for a [B][H][N][d] problem
+ * (with_lse != 0 when lse_out will be requested): reordered copies of q, k, v and o
+ * (and of the LSE).  0 for an empty problem.
+ */
+size_t dsattn_reordered_workspace_bytes(int B, int H, int N, int d, int with_lse);
+
+/*
+ * dsattn_attn_fwd_ex over a reordered sequence: queries are taken in the order q_index
+ * (a gather map, e.g. from dsattn_block_order), keys and values in the order kv_index,
+ * the key-tile loop and its skip decisions run over the reordered tiles, and o and
+ * lse_out are returned in the ORIGINAL query order.  mask_out and stats_out describe the
+ * reordered (query tile, key tile) pairs.  q_index and kv_index are device int32 [N]
+ * arrays that must be permutations of 0..N-1 (not checked; see dsattn_gather_rows for
+ * entries outside [0, N)).  workspace is a caller-owned device buffer of at least
+ * dsattn_reordered_workspace_bytes(B, H, N, d, lse_out != NULL) bytes, 256-byte aligned,
+ * overlapping none of q, k, v, o; its contents are overwritten.  Everything else as
+ * dsattn_attn_fwd_ex.
+ */
+int dsattn_attn_fwd_reordered(const dsattn_args* args, const int32_t* q_index,
+                              const int32_t* kv_index, void* workspace,
+                              size_t workspace_bytes);
 
 /* Message describing the last error on this thread ("" after a successful call). */
 const char* dsattn_last_error(void);

@@ -82,6 +82,18 @@ def lib():
         L.dsattn_attn_fwd_ex.restype = ctypes.c_int
         L.dsattn_lambda_from_recall.argtypes = [ctypes.c_float, ctypes.c_int]
         L.dsattn_lambda_from_recall.restype = ctypes.c_float
+        L.dsattn_block_order.argtypes = [ctypes.c_int] * 6 + [ctypes.c_void_p]
+        L.dsattn_block_order.restype = ctypes.c_int
+        for name in ("dsattn_gather_rows", "dsattn_scatter_rows"):
+            getattr(L, name).argtypes = [ctypes.c_void_p] * 3 + [ctypes.c_int] * 3 + [
+                ctypes.c_void_p]
+            getattr(L, name).restype = ctypes.c_int
+        L.dsattn_reordered_workspace_bytes.argtypes = [ctypes.c_int] * 5
+        L.dsattn_reordered_workspace_bytes.restype = ctypes.c_size_t
+        L.dsattn_attn_fwd_reordered.argtypes = [ctypes.POINTER(DsAttnArgs), ctypes.c_void_p,
+                                                ctypes.c_void_p, ctypes.c_void_p,
+                                                ctypes.c_size_t]
+        L.dsattn_attn_fwd_reordered.restype = ctypes.c_int
         L.dsattn_last_error.argtypes = []
         L.dsattn_last_error.restype = ctypes.c_char_p
         L.dsattn_version.argtypes = []
@@ -226,9 +238,94 @@ def dsattn_attn_fwd_ex(rule, param, q, k, v, o=None, scale=None, tile_q=TILE_Q,
     return o
 
 
+def dsattn_block_order(grid, block):
+    """Gather map (numpy int32 [T*Y*X]) of the blocked token order, computed by the
+    library's host code: position i of the reordered sequence holds token perm[i]."""
+    import numpy as np
+
+    T, Y, X = (int(g) for g in grid)
+    bt, by, bx = (int(b) for b in block)
+    n = max(T, 0) * max(Y, 0) * max(X, 0)
+    perm = np.empty(max(n, 1), dtype=np.int32)
+    rc = lib().dsattn_block_order(T, Y, X, bt, by, bx, perm.ctypes.data)
+    _check(rc, "dsattn_block_order")
+    return perm[:n]
+
+
+def _rows(src, index, dst):
+    import torch
+
+    if not isinstance(src, torch.Tensor) or not src.is_cuda or not src.is_contiguous():
+        raise ValueError("src must be a contiguous GPU tensor")
+    if src.dim() < 2:
+        raise ValueError("src must have shape [..., N, row]")
+    if index.dtype != torch.int32 or not index.is_cuda or not index.is_contiguous():
+        raise ValueError("index must be a contiguous int32 GPU tensor")
+    N = int(src.shape[-2])
+    if index.numel() != N:
+        raise ValueError(f"index must have N={N} entries (got {index.numel()})")
+    row_bytes = int(src.shape[-1]) * src.element_size()
+    bh = src.numel() // max(1, N * int(src.shape[-1]))
+    dst = torch.empty_like(src) if dst is None else dst
+    if dst.shape != src.shape or dst.dtype != src.dtype or not dst.is_contiguous():
+        raise ValueError("dst must be a contiguous tensor like src")
+    return dst, bh, N, row_bytes
+
+
+def dsattn_gather_rows(src, index, dst=None, stream=None):
+    """dst[..., i, :] = src[..., index[i], :] on the GPU; returns dst."""
+    dst, bh, N, row_bytes = _rows(src, index, dst)
+    rc = lib().dsattn_gather_rows(src.data_ptr(), dst.data_ptr(), index.data_ptr(), bh, N,
+                                  row_bytes, _stream(stream))
+    _check(rc, "dsattn_gather_rows")
+    return dst
+
+
+def dsattn_scatter_rows(src, index, dst=None, stream=None):
+    """dst[..., index[i], :] = src[..., i, :] on the GPU; returns dst."""
+    dst, bh, N, row_bytes = _rows(src, index, dst)
+    rc = lib().dsattn_scatter_rows(src.data_ptr(), dst.data_ptr(), index.data_ptr(), bh, N,
+                                   row_bytes, _stream(stream))
+    _check(rc, "dsattn_scatter_rows")
+    return dst
+
+
+def dsattn_reordered_workspace_bytes(B, H, N, d=HEAD_DIM, with_lse=False):
+    return int(lib().dsattn_reordered_workspace_bytes(B, H, N, d, int(bool(with_lse))))
+
+
+def dsattn_attn_fwd_reordered(rule, param, q, k, v, q_index, kv_index, o=None, scale=None,
+                              tile_q=TILE_Q, tile_k=TILE_K, stats_out=None, mask_out=None,
+                              lse_out=None, workspace=None, stream=None):
+    """``dsattn_attn_fwd_ex`` over queries taken in ``q_index`` order and keys/values in
+    ``kv_index`` order (int32 GPU tensors); o and lse_out come back in the original query
+    order, mask_out and stats_out describe the reordered tiles.  ``workspace`` (a uint8
+    GPU tensor) is allocated here when not given."""
+    import torch
+
+    o = _out(q, o)
+    B, H, N, d = _shape(q, k, v, o)
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    st, mk, ls = _buffers(B, H, N, stats_out, mask_out, lse_out)
+    for name, t in (("q_index", q_index), ("kv_index", kv_index)):
+        if t.dtype != torch.int32 or not t.is_cuda or not t.is_contiguous() or t.numel() != N:
+            raise ValueError(f"{name} must be a contiguous int32 GPU tensor of N={N} entries")
+    need = dsattn_reordered_workspace_bytes(B, H, N, d, lse_out is not None)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    a = DsAttnArgs(rule, param, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                   B, H, N, d, scale, tile_q, tile_k, _stream(stream), st, mk, ls)
+    rc = lib().dsattn_attn_fwd_reordered(ctypes.byref(a), q_index.data_ptr(),
+                                         kv_index.data_ptr(), workspace.data_ptr(),
+                                         workspace.numel() * workspace.element_size())
+    _check(rc, "dsattn_attn_fwd_reordered")
+    return o
+
+
 __all__ = [
     "HEAD_DIM", "TILE_Q", "TILE_K", "RULE_DENSE", "RULE_BLASST", "RULE_DYNSPARSE_RECALL",
     "RULE_DYNSPARSE_LAMBDA", "DsAttnArgs", "lib", "last_error", "dsattn_lambda_from_recall",
     "dynsparse_attn_fwd", "dynsparse_attn_fwd_lambda", "blasst_attn_fwd", "dense_attn_fwd",
-    "dsattn_attn_fwd_ex",
+    "dsattn_attn_fwd_ex", "dsattn_block_order", "dsattn_gather_rows", "dsattn_scatter_rows",
+    "dsattn_reordered_workspace_bytes", "dsattn_attn_fwd_reordered",
 ]

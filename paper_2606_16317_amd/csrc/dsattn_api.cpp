@@ -5,12 +5,14 @@
 
 #include <hip/hip_runtime_api.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <string>
 
 #include "fa_fwd_launch.h"
+#include "reorder_launch.h"
 
 namespace {
 
@@ -48,7 +50,10 @@ struct Request {
   float thr_log2;  // threshold in log2 units
 };
 
-int run(const dsattn_args& a, const Request& rq) {
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Size, scale and shape checks shared by every attention entry point.
+int check_problem(const dsattn_args& a) {
   if (a.B < 0 || a.H < 0 || a.N < 0)
     return fail(DSATTN_EINVAL, "B, H and N must be >= 0");
   if (!(a.scale > 0.f) || !std::isfinite(a.scale))
@@ -61,24 +66,23 @@ int run(const dsattn_args& a, const Request& rq) {
   if (bh > 65535) return fail(DSATTN_EINVAL, "B*H must be <= 65535 (got %lld)", bh);
   if ((long long)a.N * kHeadDim * bh > (1LL << 40))
     return fail(DSATTN_EINVAL, "problem too large");
+  return DSATTN_OK;
+}
 
-  if (bh == 0 || a.N == 0) {
-    if (a.stats_out != nullptr && bh > 0) {
-      if (!is_device_pointer(a.stats_out))
-        return fail(DSATTN_EINVAL, "stats_out is not a device pointer");
-      if (dsattn::launch_zero_u64(a.stats_out, (int)(bh * 4), a.stream) != hipSuccess)
-        return fail(DSATTN_ELAUNCH, "zero-fill launch failed");
-    }
-    g_last_error.clear();
-    return DSATTN_OK;
-  }
+bool empty_problem(const dsattn_args& a) { return a.B == 0 || a.H == 0 || a.N == 0; }
+
+// Pointer checks of a non-empty problem.
+int check_pointers(const dsattn_args& a) {
   if (a.q == nullptr || a.k == nullptr || a.v == nullptr || a.o == nullptr)
     return fail(DSATTN_EINVAL, "q, k, v and o must be non-null");
   const void* ptrs[] = {a.q, a.k, a.v, a.o};
   const char* names[] = {"q", "k", "v", "o"};
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 4; ++i) {
     if (!is_device_pointer(ptrs[i]))
       return fail(DSATTN_EINVAL, "%s is not a device pointer", names[i]);
+    if (!aligned(ptrs[i], 16))
+      return fail(DSATTN_EINVAL, "%s must be 16-byte aligned", names[i]);
+  }
   if (a.o == a.q || a.o == a.k || a.o == a.v)
     return fail(DSATTN_EINVAL, "o must not alias q, k or v");
   if (a.stats_out != nullptr && !is_device_pointer(a.stats_out))
@@ -87,7 +91,27 @@ int run(const dsattn_args& a, const Request& rq) {
     return fail(DSATTN_EINVAL, "mask_out is not a device pointer");
   if (a.lse_out != nullptr && !is_device_pointer(a.lse_out))
     return fail(DSATTN_EINVAL, "lse_out is not a device pointer");
+  if (a.lse_out != nullptr && !aligned(a.lse_out, 4))
+    return fail(DSATTN_EINVAL, "lse_out must be 4-byte aligned");
+  return DSATTN_OK;
+}
 
+// Zero stats_out of an empty problem (the only output it has).
+int finish_empty(const dsattn_args& a) {
+  const long long bh = (long long)a.B * (long long)a.H;
+  if (a.stats_out != nullptr && bh > 0) {
+    if (!is_device_pointer(a.stats_out))
+      return fail(DSATTN_EINVAL, "stats_out is not a device pointer");
+    if (dsattn::launch_zero_u64(a.stats_out, (int)(bh * 4), a.stream) != hipSuccess)
+      return fail(DSATTN_ELAUNCH, "zero-fill launch failed");
+  }
+  g_last_error.clear();
+  return DSATTN_OK;
+}
+
+// Enqueue the attention kernels of a checked, non-empty problem.
+int launch_attention(const dsattn_args& a, const Request& rq) {
+  const long long bh = (long long)a.B * (long long)a.H;
   dsattn::FwdParams p;
   p.q = static_cast<const uint16_t*>(a.q);
   p.k = static_cast<const uint16_t*>(a.k);
@@ -107,8 +131,67 @@ int run(const dsattn_args& a, const Request& rq) {
     return fail(DSATTN_ELAUNCH, "zero-fill launch failed");
   const hipError_t e = dsattn::launch_fa_fwd(rq.rule, p, (int)bh, a.stream);
   if (e != hipSuccess) return fail(DSATTN_ELAUNCH, "kernel launch failed: %s", hipGetErrorString(e));
+  return DSATTN_OK;
+}
+
+int run(const dsattn_args& a, const Request& rq) {
+  int rc = check_problem(a);
+  if (rc != DSATTN_OK) return rc;
+  if (empty_problem(a)) return finish_empty(a);
+  if ((rc = check_pointers(a)) != DSATTN_OK) return rc;
+  if ((rc = launch_attention(a, rq)) != DSATTN_OK) return rc;
   g_last_error.clear();
   return DSATTN_OK;
+}
+
+// ---- token reordering -----------------------------------------------------------------
+
+// True unless `p` is device-only memory (the host writes the block order directly).
+bool host_writable(const void* p) {
+  hipPointerAttribute_t attr;
+  if (hipPointerGetAttributes(&attr, p) != hipSuccess) {
+    (void)hipGetLastError();
+    return true;  // ordinary pageable host memory is unknown to the runtime
+  }
+  return attr.type != hipMemoryTypeDevice;
+}
+
+// Checks of a row move over [bh][N][row_bytes]; sets *wide when 16-byte chunks can be used.
+int check_rows(const void* src, const void* dst, const int32_t* index, int bh, int N,
+               int row_bytes, bool* wide) {
+  if (bh < 0 || N < 0) return fail(DSATTN_EINVAL, "BH and N must be >= 0");
+  if (bh > 65535) return fail(DSATTN_EINVAL, "BH must be <= 65535 (got %d)", bh);
+  if (row_bytes <= 0 || row_bytes % 4 != 0)
+    return fail(DSATTN_EINVAL, "row_bytes must be a positive multiple of 4 (got %d)", row_bytes);
+  if ((long long)N * (row_bytes / 4) > (1LL << 31))
+    return fail(DSATTN_EINVAL, "N * row_bytes is too large for one head");
+  if (bh == 0 || N == 0) return DSATTN_OK;
+  if (src == nullptr || dst == nullptr || index == nullptr)
+    return fail(DSATTN_EINVAL, "src, dst and index must be non-null");
+  const void* ptrs[] = {src, dst, index};
+  const char* names[] = {"src", "dst", "index"};
+  for (int i = 0; i < 3; ++i) {
+    if (!is_device_pointer(ptrs[i]))
+      return fail(DSATTN_EINVAL, "%s is not a device pointer", names[i]);
+    if (!aligned(ptrs[i], 4)) return fail(DSATTN_EINVAL, "%s must be 4-byte aligned", names[i]);
+  }
+  const uintptr_t bytes = (uintptr_t)bh * (uintptr_t)N * (uintptr_t)row_bytes;
+  const uintptr_t s0 = reinterpret_cast<uintptr_t>(src), d0 = reinterpret_cast<uintptr_t>(dst);
+  if (s0 < d0 + bytes && d0 < s0 + bytes)
+    return fail(DSATTN_EINVAL, "src and dst must not overlap");
+  *wide = row_bytes % 16 == 0 && aligned(src, 16) && aligned(dst, 16);
+  return DSATTN_OK;
+}
+
+constexpr size_t kSliceAlign = 256;
+
+size_t round_up(size_t x) { return (x + kSliceAlign - 1) / kSliceAlign * kSliceAlign; }
+
+size_t workspace_bytes(int B, int H, int N, int d, bool with_lse) {
+  if (B <= 0 || H <= 0 || N <= 0 || d <= 0) return 0;
+  const size_t bhn = (size_t)B * (size_t)H * (size_t)N;
+  const size_t slice = round_up(bhn * (size_t)d * 2);
+  return 4 * slice + (with_lse ? round_up(bhn * 4) : 0);
 }
 
 double lambda_from_recall(double r, int n) {
@@ -223,6 +306,127 @@ int dense_attn_fwd(const void* q, const void* k, const void* v, void* o, int B, 
   const dsattn_args a = make_args(DSATTN_RULE_DENSE, 0.f, q, k, v, o, B, H, N, d, scale,
                                   tile_q, tile_k, stream, stats_out);
   return dsattn_attn_fwd_ex(&a);
+}
+
+int dsattn_block_order(int T, int Y, int X, int bt, int by, int bx, int32_t* perm_out) {
+  if (T <= 0 || Y <= 0 || X <= 0 || bt <= 0 || by <= 0 || bx <= 0)
+    return fail(DSATTN_EINVAL, "grid and block extents must be positive");
+  const long long n = (long long)T * Y * X;
+  if (n > 0x7fffffffLL) return fail(DSATTN_EINVAL, "grid has more than 2^31 - 1 tokens");
+  if (perm_out == nullptr) return fail(DSATTN_EINVAL, "perm_out must be non-null");
+  if (!host_writable(perm_out)) return fail(DSATTN_EINVAL, "perm_out must be host memory");
+  // The reordered position of token (t, y, x) in closed form: the tokens of all earlier
+  // block slabs along t, then of the earlier block rows of its slab, then of the earlier
+  // blocks of its block row, then its row-major rank inside its own (possibly clipped)
+  // block.
+  const long long YX = (long long)Y * X;
+  for (int t = 0; t < T; ++t) {
+    const int t0 = t / bt * bt, et = std::min(bt, T - t0);
+    for (int y = 0; y < Y; ++y) {
+      const int y0 = y / by * by, ey = std::min(by, Y - y0);
+      for (int x = 0; x < X; ++x) {
+        const int x0 = x / bx * bx, ex = std::min(bx, X - x0);
+        const long long pos = (long long)t0 * YX + (long long)et * y0 * X +
+                              (long long)et * ey * x0 +
+                              ((long long)(t - t0) * ey + (y - y0)) * ex + (x - x0);
+        perm_out[pos] = (int32_t)((long long)t * YX + (long long)y * X + x);
+      }
+    }
+  }
+  g_last_error.clear();
+  return DSATTN_OK;
+}
+
+int dsattn_gather_rows(const void* src, void* dst, const int32_t* index, int BH, int N,
+                       int row_bytes, hipStream_t stream) {
+  bool wide = false;
+  const int rc = check_rows(src, dst, index, BH, N, row_bytes, &wide);
+  if (rc != DSATTN_OK) return rc;
+  if (BH > 0 && N > 0) {
+    const hipError_t e = dsattn::launch_gather_rows(src, dst, index, BH, N, row_bytes, wide, stream);
+    if (e != hipSuccess) return fail(DSATTN_ELAUNCH, "gather launch failed: %s", hipGetErrorString(e));
+  }
+  g_last_error.clear();
+  return DSATTN_OK;
+}
+
+int dsattn_scatter_rows(const void* src, void* dst, const int32_t* index, int BH, int N,
+                        int row_bytes, hipStream_t stream) {
+  bool wide = false;
+  const int rc = check_rows(src, dst, index, BH, N, row_bytes, &wide);
+  if (rc != DSATTN_OK) return rc;
+  if (BH > 0 && N > 0) {
+    const hipError_t e = dsattn::launch_scatter_rows(src, dst, index, BH, N, row_bytes, wide, stream);
+    if (e != hipSuccess) return fail(DSATTN_ELAUNCH, "scatter launch failed: %s", hipGetErrorString(e));
+  }
+  g_last_error.clear();
+  return DSATTN_OK;
+}
+
+size_t dsattn_reordered_workspace_bytes(int B, int H, int N, int d, int with_lse) {
+  return workspace_bytes(B, H, N, d, with_lse != 0);
+}
+
+int dsattn_attn_fwd_reordered(const dsattn_args* args, const int32_t* q_index,
+                              const int32_t* kv_index, void* workspace,
+                              size_t workspace_size) {
+  if (args == nullptr) return fail(DSATTN_EINVAL, "args must be non-null");
+  const dsattn_args& a = *args;
+  Request rq;
+  int rc = resolve_request(a, &rq);
+  if (rc != DSATTN_OK) return rc;
+  if ((rc = check_problem(a)) != DSATTN_OK) return rc;
+  if (empty_problem(a)) return finish_empty(a);
+  if ((rc = check_pointers(a)) != DSATTN_OK) return rc;
+  if (q_index == nullptr || kv_index == nullptr || workspace == nullptr)
+    return fail(DSATTN_EINVAL, "q_index, kv_index and workspace must be non-null");
+  if (!is_device_pointer(q_index) || !is_device_pointer(kv_index))
+    return fail(DSATTN_EINVAL, "q_index and kv_index must be device pointers");
+  if (!aligned(q_index, 4) || !aligned(kv_index, 4))
+    return fail(DSATTN_EINVAL, "q_index and kv_index must be 4-byte aligned");
+  if (!is_device_pointer(workspace)) return fail(DSATTN_EINVAL, "workspace is not a device pointer");
+  if (!aligned(workspace, kSliceAlign))
+    return fail(DSATTN_EINVAL, "workspace must be %zu-byte aligned", kSliceAlign);
+  const bool with_lse = a.lse_out != nullptr;
+  const size_t need = workspace_bytes(a.B, a.H, a.N, a.d, with_lse);
+  if (workspace_size < need)
+    return fail(DSATTN_EINVAL, "workspace too small: %zu bytes given, %zu needed", workspace_size, need);
+
+  const int bh = a.B * a.H;
+  const size_t slice = round_up((size_t)bh * (size_t)a.N * (size_t)a.d * 2);
+  char* ws = static_cast<char*>(workspace);
+  const uintptr_t w0 = reinterpret_cast<uintptr_t>(ws), w1 = w0 + need;
+  const size_t tensor_bytes = (size_t)bh * (size_t)a.N * (size_t)a.d * 2;
+  const void* io[] = {a.q, a.k, a.v, a.o};
+  for (const void* p : io) {
+    const uintptr_t p0 = reinterpret_cast<uintptr_t>(p);
+    if (p0 < w1 && w0 < p0 + tensor_bytes)
+      return fail(DSATTN_EINVAL, "workspace must not overlap q, k, v or o");
+  }
+  dsattn_args r = a;  // the same problem over the reordered sequence
+  r.q = ws;
+  r.k = ws + slice;
+  r.v = ws + 2 * slice;
+  r.o = ws + 3 * slice;
+  r.lse_out = with_lse ? reinterpret_cast<float*>(ws + 4 * slice) : nullptr;
+  const int row = a.d * 2;
+  const struct {
+    const void* src;
+    const void* dst;
+    const int32_t* index;
+  } gathers[] = {{a.q, r.q, q_index}, {a.k, r.k, kv_index}, {a.v, r.v, kv_index}};
+  for (const auto& g : gathers) {
+    const hipError_t e = dsattn::launch_gather_rows(g.src, const_cast<void*>(g.dst), g.index, bh,
+                                                    a.N, row, true, a.stream);
+    if (e != hipSuccess) return fail(DSATTN_ELAUNCH, "gather launch failed: %s", hipGetErrorString(e));
+  }
+  if ((rc = launch_attention(r, rq)) != DSATTN_OK) return rc;
+  hipError_t e = dsattn::launch_scatter_rows(r.o, a.o, q_index, bh, a.N, row, true, a.stream);
+  if (e == hipSuccess && with_lse)
+    e = dsattn::launch_scatter_rows(r.lse_out, a.lse_out, q_index, bh, a.N, 4, false, a.stream);
+  if (e != hipSuccess) return fail(DSATTN_ELAUNCH, "scatter launch failed: %s", hipGetErrorString(e));
+  g_last_error.clear();
+  return DSATTN_OK;
 }
 
 const char* dsattn_last_error(void) { return g_last_error.c_str(); }

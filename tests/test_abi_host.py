@@ -34,7 +34,9 @@ def test_header_declares_the_entry_points():
     names = declared_functions()
     for n in ("dynsparse_attn_fwd", "dynsparse_attn_fwd_lambda", "blasst_attn_fwd",
               "dense_attn_fwd", "dsattn_attn_fwd_ex", "dsattn_lambda_from_recall",
-              "dsattn_last_error", "dsattn_version"):
+              "dsattn_last_error", "dsattn_version", "dsattn_block_order",
+              "dsattn_gather_rows", "dsattn_scatter_rows", "dsattn_reordered_workspace_bytes",
+              "dsattn_attn_fwd_reordered"):
         assert n in names
 
 
@@ -55,13 +57,10 @@ def test_struct_mirror_matches_header_field_order():
         decl = decl.strip()
         if not decl:
             continue
-        toks = decl.replace("*", " ").split()
         if "," in decl:
-            first = toks[-1] if "," not in toks[-1] else None
-            parts = [p.strip().replace("*", "").split()[-1] for p in decl.split(",")]
-            fields += parts
+            fields += [p.strip().replace("*", "").split()[-1] for p in decl.split(",")]
         else:
-            fields.append(toks[-1])
+            fields.append(decl.replace("*", " ").split()[-1])
     assert fields == [f[0] for f in pkg.DsAttnArgs._fields_]
 
 
@@ -155,3 +154,83 @@ def test_empty_problem_is_a_no_op():
 def test_version_string():
     pkg = _lib()
     assert b"gfx950" in pkg.lib().dsattn_version()
+
+
+# ---- token reordering (host side) ---------------------------------------------------------
+
+@pytest.mark.parametrize("grid,block", [((1, 3, 3), (1, 2, 2)), ((21, 45, 80), (2, 8, 8)),
+                                        ((21, 45, 80), (1, 8, 8)), ((3, 5, 7), (2, 3, 4)),
+                                        ((32, 64, 64), (1, 8, 8)), ((2, 32, 32), (5, 7, 9))])
+def test_block_order_matches_oracle(grid, block):
+    """The library's closed-form block order equals the oracle's enumeration, bit for bit."""
+    import numpy as np
+    from oracle.reorder import block_order
+
+    pkg = _lib()
+    got = pkg.dsattn_block_order(grid, block)
+    assert got.dtype == np.int32
+    assert np.array_equal(got.astype(np.int64), block_order(grid, block))
+
+
+@pytest.mark.parametrize("args,msg", [
+    ((0, 2, 2, 1, 1, 1), "positive"),
+    ((2, 2, 2, 1, -1, 1), "positive"),
+    ((2048, 2048, 1024, 1, 1, 1), "2^31"),
+])
+def test_block_order_rejects_bad_extents(args, msg):
+    import numpy as np
+
+    pkg = _lib()
+    buf = np.zeros(16, dtype=np.int32)
+    rc = pkg.lib().dsattn_block_order(*args, buf.ctypes.data)
+    assert rc == -1 and msg in pkg.last_error()
+    assert pkg.lib().dsattn_block_order(2, 2, 2, 1, 1, 1, None) == -1
+
+
+@pytest.mark.parametrize("name", ["dsattn_gather_rows", "dsattn_scatter_rows"])
+@pytest.mark.parametrize("bh,n,row,msg", [
+    (1, 4, 6, "multiple of 4"), (1, 4, 0, "multiple of 4"), (-1, 4, 16, ">= 0"),
+    (70000, 4, 16, "65535"), (1, 1 << 30, 64, "too large"), (1, 4, 16, "non-null"),
+])
+def test_row_moves_reject_bad_arguments(name, bh, n, row, msg):
+    rc, err = _call_raw(name, None, None, None, bh, n, row, None)
+    assert rc == -1 and msg in err
+
+
+@pytest.mark.parametrize("name", ["dsattn_gather_rows", "dsattn_scatter_rows"])
+def test_row_moves_reject_host_pointers_and_accept_empty(name):
+    buf = (ctypes.c_uint32 * 64)()
+    p = ctypes.addressof(buf)
+    rc, err = _call_raw(name, p, p + 128, p, 1, 4, 16, None)
+    assert rc == -1 and "device pointer" in err
+    rc, err = _call_raw(name, None, None, None, 0, 4, 16, None)
+    assert rc == 0 and err == ""
+
+
+def test_reordered_workspace_size():
+    pkg = _lib()
+    L = pkg.lib()
+    tensor = 1 * 40 * 75600 * 128 * 2
+    slice_ = -(-tensor // 256) * 256
+    assert L.dsattn_reordered_workspace_bytes(1, 40, 75600, 128, 0) == 4 * slice_
+    lse = -(-(40 * 75600 * 4) // 256) * 256
+    assert L.dsattn_reordered_workspace_bytes(1, 40, 75600, 128, 1) == 4 * slice_ + lse
+    assert L.dsattn_reordered_workspace_bytes(0, 40, 75600, 128, 1) == 0
+    assert L.dsattn_reordered_workspace_bytes(1, 3, 100, 128, 0) == 4 * (-(-(3 * 100 * 256) // 256) * 256)
+
+
+def test_reordered_rejects_bad_arguments():
+    pkg = _lib()
+    L = pkg.lib()
+    assert L.dsattn_attn_fwd_reordered(None, None, None, None, 0) == -1
+    a = pkg.DsAttnArgs(pkg.RULE_DYNSPARSE_LAMBDA, float("nan"), None, None, None, None, 1, 1,
+                       16, 128, 0.1, 128, 64, None, None, None, None)
+    assert L.dsattn_attn_fwd_reordered(ctypes.byref(a), None, None, None, 0) == -1
+    assert "lambda" in pkg.last_error()
+    a.param = -6.0
+    assert L.dsattn_attn_fwd_reordered(ctypes.byref(a), None, None, None, 0) == -1
+    assert "non-null" in pkg.last_error()
+    a.tile_q = 64
+    assert L.dsattn_attn_fwd_reordered(ctypes.byref(a), None, None, None, 0) == -2
+    a.tile_q, a.N = 128, 0
+    assert L.dsattn_attn_fwd_reordered(ctypes.byref(a), None, None, None, 0) == 0
