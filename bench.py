@@ -10,7 +10,10 @@ d=128, bf16), with the inputs already resident in HBM.  ``value`` is the effecti
 the work it actually issues, and times the fp64 CPU oracle on a bounded sample of the
 same layer as a reference point.  One JSON line is printed.
 
-``--sweep`` instead prints one JSON line per rule/threshold on the given workload.
+``--sweep`` instead prints one JSON line per rule/threshold on the given workload;
+``--reorder-sweep`` prints, per rule/threshold, the row-major run next to the same run over
+the spatio-temporally blocked token order (``dsattn_attn_fwd_reordered``, gathers and the
+output scatter included in its time), plus the HBM rate of the row gather kernel.
 """
 
 from __future__ import annotations
@@ -43,6 +46,10 @@ def parse():
                     help="approximate CPU budget of the oracle baseline (0 = skip)")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense timing (profiling)")
     ap.add_argument("--sweep", action="store_true", help="one line per rule/threshold")
+    ap.add_argument("--reorder-sweep", action="store_true",
+                    help="row-major vs blocked token order, one line per rule/threshold")
+    ap.add_argument("--q-block", default="2,8,8", help="query block (t,y,x) for --reorder-sweep")
+    ap.add_argument("--kv-block", default="1,8,8", help="key/value block for --reorder-sweep")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run a plain 1 GiB -> 1 GiB copy kernel (HBM counter calibration)")
     ap.add_argument("--no-gemm-ref", action="store_true",
@@ -243,6 +250,8 @@ def main():
 
     if args.sweep:
         return sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop)
+    if args.reorder_sweep:
+        return reorder_sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop)
 
     def step():
         dsa.dynsparse_attn_fwd(qd, kd, vd, o, scale=scale, recall_target=recall, stats_out=stats)
@@ -353,6 +362,57 @@ def sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop):
                "actual_tflops": algorithmic_flops(st) / (ms * 1e-3) / 1e12,
                "sparsity_tiles": float(st[:, 1].sum() / st[:, 0].sum()),
                "speedup_vs_dense": dense_ms / ms, "rel_l2_vs_dense": rel}
+        print(json.dumps(rec), flush=True)
+
+
+def reorder_sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop):
+    import torch
+
+    B, H, N = w.B, w.H, w.N
+    qb = tuple(int(x) for x in args.q_block.split(","))
+    kb = tuple(int(x) for x in args.kv_block.split(","))
+    q_idx = torch.from_numpy(dsa.dsattn_block_order(w.grid, qb)).cuda()
+    kv_idx = torch.from_numpy(dsa.dsattn_block_order(w.grid, kb)).cuda()
+    ws = torch.empty(dsa.dsattn_reordered_workspace_bytes(B, H, N, D), dtype=torch.uint8,
+                     device="cuda")
+
+    # row gather kernel alone: one [B,H,N,128] bf16 tensor, read once and written once
+    g = torch.empty_like(qd)
+    ms = time_calls(lambda: dsa.dsattn_gather_rows(qd, q_idx, g), args.steps, args.warmup)
+    moved = 2 * B * H * N * D * 2 + N * 4
+    del g
+    print(json.dumps({"workload": w.name, "kernel": "gather_rows", "ms": ms,
+                      "roofline": {"bound": "hbm", "achieved": moved / (ms * 1e-3) / 1e9,
+                                   "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                   "frac": moved / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}}),
+          flush=True)
+
+    rules = {"dense": dsa.RULE_DENSE, "dynsparse_recall": dsa.RULE_DYNSPARSE_RECALL,
+             "dynsparse_lambda": dsa.RULE_DYNSPARSE_LAMBDA, "blasst": dsa.RULE_BLASST}
+    points = [("dense", 0.0), ("dynsparse_recall", 0.95), ("dynsparse_lambda", -10.0),
+              ("dynsparse_lambda", -8.0), ("dynsparse_lambda", -6.0), ("blasst", 1e-2)]
+    dense_ms = None
+    for rule, p in points:
+        rec = {"workload": w.name, "rule": rule, "param": p, "q_block": qb, "kv_block": kb}
+        for order in ("row_major", "blocked"):
+            if order == "row_major":
+                fn = lambda: dsa.dsattn_attn_fwd_ex(rules[rule], p, qd, kd, vd, o, scale=scale,
+                                                    stats_out=stats)
+            else:
+                fn = lambda: dsa.dsattn_attn_fwd_reordered(rules[rule], p, qd, kd, vd, q_idx,
+                                                           kv_idx, o, scale=scale,
+                                                           stats_out=stats, workspace=ws)
+            print(f"[reorder-sweep] {rule} {p} {order}", file=sys.stderr, flush=True)
+            ms = time_calls(fn, args.steps, args.warmup)
+            st = stats.cpu().numpy().reshape(B * H, 4)
+            if rule == "dense" and order == "row_major":
+                dense_ms = ms
+                od.copy_(o)
+            rel = float((o.float() - od.float()).pow(2).sum().sqrt() /
+                        od.float().pow(2).sum().sqrt())
+            rec[order] = {"ms": ms, "effective_tflops": dense_flop / (ms * 1e-3) / 1e12,
+                          "sparsity_tiles": float(st[:, 1].sum() / st[:, 0].sum()),
+                          "speedup_vs_dense": dense_ms / ms, "rel_l2_vs_dense": rel}
         print(json.dumps(rec), flush=True)
 
 

@@ -145,6 +145,20 @@ __device__ __forceinline__ uint32_t tile_lane_offset(int w, int lane) {
   return (uint32_t)(key * (kD * 2) + chunk * 16);
 }
 
+__device__ __forceinline__ uint32_t v_lane_offset(int w, int lane) {
+  return tile_lane_offset<true>(w, lane);
+}
+
+// The whole V tile starting at key `key0`, fetched by one wave (sixteen 1 KiB blocks: the
+// four-block shares of all four waves).  Used when a tile's V is requested in its own
+// iteration: every wave fetches the same bytes into the same places, so each wave only
+// has to wait for its own transfers before reading the tile, and no barrier is needed.
+__device__ __forceinline__ void load_v_tile_whole(uint16_t* tile, __amdgpu_buffer_rsrc_t rs,
+                                                  int key0, int lane) {
+#pragma unroll
+  for (int w = 0; w < 4; ++w) load_tile_lds(tile, rs, v_lane_offset(w, lane), key0, w);
+}
+
 __device__ __forceinline__ bf16x8 lds_b128(const uint16_t* p) {
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p));
 }
@@ -249,6 +263,13 @@ __device__ __forceinline__ void kept_tile(RowState& rs, f32x16 (&o)[4], const f3
   __builtin_amdgcn_s_setprio(1);
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
+    if (i == 14) {
+      // Before the first V_j read, this wave's transfers older than the newest eight
+      // (V_{j+1} and K_{j+2}, four each) must have landed.  That is a no-op when V_j was
+      // prefetched an iteration ago; when it was requested late in this iteration, this
+      // wave fetched the whole tile itself, so its own count is all it waits for.
+      asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    }
     if (i + 2 < 16)
       ka[(i + 2) % 3] = k_operand(kt, i + 2, r, g);
     else
@@ -314,23 +335,32 @@ struct SkipCount {
   uint64_t elems = 0;
 };
 
-// One key tile j.  On entry s_cur holds S_j, mhat its row max (log2 units) and keep the
-// workgroup's decision for tile j.  On exit s_next holds S_{j+1}, mhat / keep refer to
-// tile j+1, and every wave has passed the barrier that publishes the K_{j+2} / V_{j+1}
-// buffers and the tile-(j+1) votes.
+// One key tile j.  On entry s_cur holds S_j, mhat its row max (log2 units), keep the
+// workgroup's decision for tile j, and v_ready says whether V_j is already in LDS
+// (buffer j % 2).  On exit s_next holds S_{j+1}, mhat / keep / v_ready refer to tile j+1,
+// and every wave has passed the barrier that publishes K_{j+2}, the V_{j+1} buffer if it
+// was requested, and the tile-(j+1) votes.
+//
+// V tiles are fetched for kept tiles only.  V_{j+1} is requested one iteration ahead when
+// tile j is kept (runs of kept tiles are the common case); after a skipped tile, a kept
+// tile's V is requested at the start of its own iteration (by every wave in full) and
+// waited for just before its P.V product, so a run of skipped tiles streams K alone.
 template <int RULE>
 __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f32x16 (&s_next)[2],
-                                              float& mhat, bool& keep, RowState& rs,
-                                              f32x16 (&o)[4], const bf16x8 (&qf)[8], Smem& sm,
+                                              float& mhat, bool& keep, bool& v_ready,
+                                              RowState& rs, f32x16 (&o)[4],
+                                              const bf16x8 (&qf)[8], Smem& sm,
                                               const LoopCtx& cx, SkipCount& sk) {
   const int nb = (j + 1) & 1;
   const bool has_next = (j + 1) < cx.n_kt;
-  // Issued unconditionally: past the last tile the range check returns zeros into
-  // buffers nobody reads, and the loop body stays free of branches here.
-  load_tile_lds(sm.v[nb], cx.vrs, cx.voff, (j + 1) * kTK, cx.w);
-  load_tile_lds(sm.k[j & 1], cx.krs, cx.koff, (j + 2) * kTK, cx.w);
-
   if (cx.mask_row != nullptr && cx.w == 0 && cx.lane == 0) cx.mask_row[j] = keep ? 0 : 1;
+
+  // Tile loads, oldest first (the late-V wait counts the transfers issued after V_j).
+  // Past the last tile the range check returns zeros into buffers nobody reads.
+  const bool late_v = keep && !v_ready;
+  if (late_v) load_v_tile_whole(sm.v[j & 1], cx.vrs, j * kTK, cx.lane);
+  if (keep) load_tile_lds(sm.v[nb], cx.vrs, cx.voff, (j + 1) * kTK, cx.w);
+  load_tile_lds(sm.k[j & 1], cx.krs, cx.koff, (j + 2) * kTK, cx.w);
 
   // S_{j+1} is computed on both paths (on the last tile it reads a stale buffer and is
   // dropped).
@@ -341,6 +371,7 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
     sk.elems += (uint64_t)cx.rows_valid * (uint64_t)min(kTK, cx.N - j * kTK);
     skipped_tile(s_next, sm.k[nb], qf, cx.r, cx.g);
   }
+  v_ready = keep;
 
   float mhat_next = 0.f;
   if (has_next) {
@@ -351,9 +382,9 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
       if (cx.lane == 0) sm.vote[nb][cx.w] = wave_keeps ? 1 : 0;
     }
   }
-  // Publish this wave's LDS traffic and its V_{j+1} / K_{j+2} tile loads (both are read
-  // in the next iteration), then meet the other waves.  (__syncthreads() would add a
-  // fence that makes the compiler drain every load again on its own.)
+  // Publish this wave's LDS traffic and its tile loads (read in the next iteration), then
+  // meet the other waves.  (__syncthreads() would add a fence that makes the compiler
+  // drain every load again on its own.)
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
   if (has_next) {
     if constexpr (RULE != kRuleDense)
@@ -424,13 +455,15 @@ fa_fwd_kernel(FwdParams p) {
   if (cx.ragged && cx.n_kt == 1) mask_tail(sa, 0, N, cx.g);
   float mhat = row_max(sa) * cx.c;
   bool keep = true;                          // the first tile is always kept
+  bool v_ready = true;                       // V_0 was staged above
   SkipCount sk;
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");  // K_0 consumed
 
   // Unrolled by two so that S_j / S_{j+1} alternate between sa and sb without copies.
   for (int j = 0; j < cx.n_kt; j += 2) {
-    key_tile_step<RULE>(j, sa, sb, mhat, keep, rs, o, qf, sm, cx, sk);
-    if (j + 1 < cx.n_kt) key_tile_step<RULE>(j + 1, sb, sa, mhat, keep, rs, o, qf, sm, cx, sk);
+    key_tile_step<RULE>(j, sa, sb, mhat, keep, v_ready, rs, o, qf, sm, cx, sk);
+    if (j + 1 < cx.n_kt)
+      key_tile_step<RULE>(j + 1, sb, sa, mhat, keep, v_ready, rs, o, qf, sm, cx, sk);
   }
 
   // ---- epilogue: renormalise over kept keys, store O (bf16) and the row LSE --------
