@@ -145,19 +145,6 @@ __device__ __forceinline__ uint32_t tile_lane_offset(int w, int lane) {
   return (uint32_t)(key * (kD * 2) + chunk * 16);
 }
 
-__device__ __forceinline__ uint32_t v_lane_offset(int w, int lane) {
-  return tile_lane_offset<true>(w, lane);
-}
-
-// The whole V tile starting at key `key0`, fetched by one wave (sixteen 1 KiB blocks: the
-// four-block shares of all four waves).  Used when a tile's V is requested in its own
-// iteration: every wave fetches the same bytes into the same places, so each wave only
-// has to wait for its own transfers before reading the tile, and no barrier is needed.
-__device__ __forceinline__ void load_v_tile_whole(uint16_t* tile, __amdgpu_buffer_rsrc_t rs,
-                                                  int key0, int lane) {
-#pragma unroll
-  for (int w = 0; w < 4; ++w) load_tile_lds(tile, rs, v_lane_offset(w, lane), key0, w);
-}
 
 __device__ __forceinline__ bf16x8 lds_b128(const uint16_t* p) {
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p));
@@ -247,7 +234,10 @@ __device__ __forceinline__ void softmax_elem(const f32x16 (&st)[2], int e, float
 }
 
 // Kept tile j: softmax of S_j interleaved with the 16 MFMAs of S_{j+1} = K_{j+1} Q^T,
-// then O += P V_j.  MFMA operands are read from LDS two MFMAs ahead.
+// then O += P V_j.  MFMA operands are read from LDS two MFMAs ahead.  kLateV: V_j may
+// have been requested in this iteration (rule kernels; the dense kernel always has it a
+// tile ahead).
+template <bool kLateV>
 __device__ __forceinline__ void kept_tile(RowState& rs, f32x16 (&o)[4], const f32x16 (&s_cur)[2],
                                           float m_hat, float c, f32x16 (&s_next)[2],
                                           const uint16_t* kt, const uint16_t* vt,
@@ -263,12 +253,12 @@ __device__ __forceinline__ void kept_tile(RowState& rs, f32x16 (&o)[4], const f3
   __builtin_amdgcn_s_setprio(1);
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
-    if (i == 14) {
-      // Before the first V_j read, this wave's transfers older than the newest eight
-      // (V_{j+1} and K_{j+2}, four each) must have landed.  That is a no-op when V_j was
-      // prefetched an iteration ago; when it was requested late in this iteration, this
-      // wave fetched the whole tile itself, so its own count is all it waits for.
-      asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    if (kLateV && i == 14) {
+      // Before the first V_j read: this wave's transfers older than the newest eight
+      // (V_{j+1} and K_{j+2}, four each) have landed, which includes its share of V_j
+      // when V_j was requested in this iteration; the barrier covers the other waves'
+      // shares.  Both are taken on every kept tile, which costs less than a branch.
+      asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
     }
     if (i + 2 < 16)
       ka[(i + 2) % 3] = k_operand(kt, i + 2, r, g);
@@ -343,8 +333,8 @@ struct SkipCount {
 //
 // V tiles are fetched for kept tiles only.  V_{j+1} is requested one iteration ahead when
 // tile j is kept (runs of kept tiles are the common case); after a skipped tile, a kept
-// tile's V is requested at the start of its own iteration (by every wave in full) and
-// waited for just before its P.V product, so a run of skipped tiles streams K alone.
+// tile's V is requested at the start of its own iteration and waited for just before its
+// P.V product, so a run of skipped tiles streams K alone.
 template <int RULE>
 __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f32x16 (&s_next)[2],
                                               float& mhat, bool& keep, bool& v_ready,
@@ -358,14 +348,15 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
   // Tile loads, oldest first (the late-V wait counts the transfers issued after V_j).
   // Past the last tile the range check returns zeros into buffers nobody reads.
   const bool late_v = keep && !v_ready;
-  if (late_v) load_v_tile_whole(sm.v[j & 1], cx.vrs, j * kTK, cx.lane);
+  if (late_v) load_tile_lds(sm.v[j & 1], cx.vrs, cx.voff, j * kTK, cx.w);
   if (keep) load_tile_lds(sm.v[nb], cx.vrs, cx.voff, (j + 1) * kTK, cx.w);
   load_tile_lds(sm.k[j & 1], cx.krs, cx.koff, (j + 2) * kTK, cx.w);
 
   // S_{j+1} is computed on both paths (on the last tile it reads a stale buffer and is
   // dropped).
   if (keep) {
-    kept_tile(rs, o, s_cur, mhat, cx.c, s_next, sm.k[nb], sm.v[j & 1], qf, cx.r, cx.g, cx.lane);
+    kept_tile<RULE != kRuleDense>(rs, o, s_cur, mhat, cx.c, s_next, sm.k[nb], sm.v[j & 1], qf,
+                                  cx.r, cx.g, cx.lane);
   } else {
     sk.tiles += 1;
     sk.elems += (uint64_t)cx.rows_valid * (uint64_t)min(kTK, cx.N - j * kTK);
