@@ -128,8 +128,8 @@ typedef struct dsattn_args {
 int dsattn_attn_fwd_ex(const dsattn_args* args);
 
 /*
- * Spatio-temporal token reordering (Section 3.2, closing remark on hyperparameter
- * selection; Section 2 describes the same grouping of tokens that are near in time and
+ * Spatio-temporal token reordering (Section 3.1, closing remark on hyperparameter
+ * selection; Section 1 describes the same grouping of tokens that are near in time and
  * space).  A video transformer flattens its T x Y x X latent grid row-major (x fastest),
  * so a 128-token query tile spans whole rows of x and a key tile's neighbours in y and t
  * lie far away in the sequence.  Regrouping the tokens into bt x by x bx blocks before the

@@ -3,9 +3,9 @@
 TEST INFRASTRUCTURE ONLY (same rule as ``oracle.attention``: imported by ``tests/``,
 ``__graft_entry__.smoke()`` and ``bench.py``'s CPU baseline leg only).
 
-Section 3.2 (hyperparameter selection, last paragraph) notes that mapping the flattened
-token sequence back to its spatio-temporal layout before the attention raises the
-correlation inside a tile; Section 2 (related work) describes the same grouping of tokens
+Section 3.1 (end of the hyperparameter-selection paragraph) notes that mapping the
+flattened token sequence back to its spatio-temporal layout before the attention raises
+the correlation inside a tile; Section 1 (related work) describes the same grouping of tokens
 that are close in time and space into one block.  The paper fixes no block shape, so the
 order is parameterised by one: the T x Y x X latent grid (tokens row-major, x fastest) is
 cut into blocks of bt x by x bx grid points (the last block along an axis may be

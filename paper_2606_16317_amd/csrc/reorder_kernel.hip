@@ -1,6 +1,7 @@
 // Row gather / scatter over the sequence axis, for the spatio-temporal token reordering
-// that precedes the attention loop (Section 3.2, last paragraph: tokens are regrouped by
-// their position in the latent video so that a tile holds neighbours in time and space).
+// that precedes the attention loop (Section 3.1, end of the hyperparameter paragraph:
+// tokens are regrouped by their position in the latent video so that a tile holds
+// neighbours in time and space).
 //
 // A tensor [BH][N][row_bytes] is moved row by row:
 //   gather:  dst[bh][i] = src[bh][index[i]]
