@@ -332,23 +332,29 @@ def sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop):
     import torch
 
     B, H, N = w.B, w.H, w.N
-    points = [("dense", None)] + [("dynsparse_recall", r) for r in (0.90, 0.95, 0.98, 0.99)] + \
-             [("dynsparse_lambda", l) for l in (-6.0, -8.0, -10.0)] + \
-             [("blasst", t) for t in (1e-2, 1e-3, 1e-4)]
+    # 128-row decisions (the default), then the same rule with every wave's 32 rows
+    # deciding on their own (tile_q = 32).
+    points = [("dense", None, TILE_Q)] + \
+             [("dynsparse_recall", r, TILE_Q) for r in (0.90, 0.95, 0.98, 0.99)] + \
+             [("dynsparse_lambda", l, TILE_Q) for l in (-6.0, -8.0, -10.0)] + \
+             [("blasst", t, TILE_Q) for t in (1e-2, 1e-3, 1e-4)] + \
+             [("dynsparse_recall", 0.95, 32), ("dynsparse_lambda", -6.0, 32),
+              ("dynsparse_lambda", -8.0, 32), ("dynsparse_lambda", -10.0, 32),
+              ("blasst", 1e-2, 32)]
     dense_ms = None
-    for rule, p in points:
+    for rule, p, tq in points:
         if rule == "dense":
             fn = lambda: dsa.dense_attn_fwd(qd, kd, vd, od, scale=scale, stats_out=stats)
         elif rule == "dynsparse_recall":
             fn = lambda: dsa.dynsparse_attn_fwd(qd, kd, vd, o, scale=scale, recall_target=p,
-                                                stats_out=stats)
+                                                tile_q=tq, stats_out=stats)
         elif rule == "dynsparse_lambda":
             fn = lambda: dsa.dynsparse_attn_fwd_lambda(qd, kd, vd, o, scale=scale, lam=p,
-                                                       stats_out=stats)
+                                                       tile_q=tq, stats_out=stats)
         else:
             fn = lambda: dsa.blasst_attn_fwd(qd, kd, vd, o, scale=scale, threshold=p,
-                                             stats_out=stats)
-        print(f"[sweep] {rule} {p}", file=sys.stderr, flush=True)
+                                             tile_q=tq, stats_out=stats)
+        print(f"[sweep] {rule} {p} tile_q={tq}", file=sys.stderr, flush=True)
         ms = time_calls(fn, args.steps, args.warmup)
         st = stats.cpu().numpy().reshape(B * H, 4)
         if rule == "dense":
@@ -357,7 +363,7 @@ def sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop):
         else:
             rel = float((o.float() - od.float()).pow(2).sum().sqrt() /
                         od.float().pow(2).sum().sqrt())
-        rec = {"workload": w.name, "rule": rule, "param": p, "ms": ms,
+        rec = {"workload": w.name, "rule": rule, "param": p, "tile_q": tq, "ms": ms,
                "effective_tflops": dense_flop / (ms * 1e-3) / 1e12,
                "actual_tflops": algorithmic_flops(st) / (ms * 1e-3) / 1e12,
                "sparsity_tiles": float(st[:, 1].sum() / st[:, 0].sum()),

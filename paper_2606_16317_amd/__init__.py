@@ -8,7 +8,8 @@ fallback: if the library is missing or a call fails, a RuntimeError is raised.
 Tensor conventions: q, k, v, o are contiguous bf16 tensors of shape [B, H, N, 128];
 ``stats_out`` is an int64 tensor of B*H*4 elements (uint64 counters
 {tiles_total, tiles_skipped, elems_total, elems_skipped} per head); ``mask_out`` is a
-uint8 tensor of B*H*ceil(N/128)*ceil(N/64) elements; ``lse_out`` a float32 tensor of
+uint8 tensor of B*H*ceil(N/tile_q)*ceil(N/64) elements (tile_q = 128, or 32 for per-wave
+decisions); ``lse_out`` a float32 tensor of
 B*H*N elements.
 """
 
@@ -159,10 +160,10 @@ def _out(q, o):
     return torch.empty_like(q) if o is None else o
 
 
-def _buffers(B, H, N, stats_out, mask_out=None, lse_out=None):
+def _buffers(B, H, N, stats_out, mask_out=None, lse_out=None, tile_q=TILE_Q):
     import torch
 
-    n_qt = -(-N // TILE_Q)
+    n_qt = -(-N // max(1, tile_q))
     n_kt = -(-N // TILE_K)
     return (_ptr(stats_out, B * H * 4, (torch.int64, torch.uint64), "stats_out"),
             _ptr(mask_out, B * H * n_qt * n_kt, (torch.uint8,), "mask_out"),
@@ -231,7 +232,7 @@ def dsattn_attn_fwd_ex(rule, param, q, k, v, o=None, scale=None, tile_q=TILE_Q,
     o = _out(q, o)
     B, H, N, d = _shape(q, k, v, o)
     scale = 1.0 / math.sqrt(d) if scale is None else scale
-    st, mk, ls = _buffers(B, H, N, stats_out, mask_out, lse_out)
+    st, mk, ls = _buffers(B, H, N, stats_out, mask_out, lse_out, tile_q)
     a = DsAttnArgs(rule, param, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
                    B, H, N, d, scale, tile_q, tile_k, _stream(stream), st, mk, ls)
     _check(lib().dsattn_attn_fwd_ex(ctypes.byref(a)), "dsattn_attn_fwd_ex")
@@ -306,7 +307,7 @@ def dsattn_attn_fwd_reordered(rule, param, q, k, v, q_index, kv_index, o=None, s
     o = _out(q, o)
     B, H, N, d = _shape(q, k, v, o)
     scale = 1.0 / math.sqrt(d) if scale is None else scale
-    st, mk, ls = _buffers(B, H, N, stats_out, mask_out, lse_out)
+    st, mk, ls = _buffers(B, H, N, stats_out, mask_out, lse_out, tile_q)
     for name, t in (("q_index", q_index), ("kv_index", kv_index)):
         if t.dtype != torch.int32 or not t.is_cuda or not t.is_contiguous() or t.numel() != N:
             raise ValueError(f"{name} must be a contiguous int32 GPU tensor of N={N} entries")

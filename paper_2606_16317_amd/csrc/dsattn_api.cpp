@@ -21,6 +21,7 @@ thread_local std::string g_last_error;
 constexpr int kHeadDim = 128;
 constexpr int kTileQ = 128;
 constexpr int kTileK = 64;
+constexpr int kUnitWave = 32;  // tile_q = 32: each wave's 32 rows decide on their own
 constexpr double kLog2e = 1.4426950408889634074;
 
 __attribute__((format(printf, 2, 3))) int fail(int code, const char* fmt, ...) {
@@ -60,8 +61,10 @@ int check_problem(const dsattn_args& a) {
     return fail(DSATTN_EINVAL, "scale must be finite and > 0 (got %g)", (double)a.scale);
   if (a.d != kHeadDim)
     return fail(DSATTN_EUNSUPPORTED, "head dimension %d is not supported (only 128)", a.d);
-  if (a.tile_q != kTileQ || a.tile_k != kTileK)
-    return fail(DSATTN_EUNSUPPORTED, "tile shape %d x %d is not supported (only 128 x 64)", a.tile_q, a.tile_k);
+  if ((a.tile_q != kTileQ && a.tile_q != kUnitWave) || a.tile_k != kTileK)
+    return fail(DSATTN_EUNSUPPORTED,
+                "tile shape %d x %d is not supported (128 x 64, or 32 x 64 for per-wave decisions)",
+                a.tile_q, a.tile_k);
   const long long bh = (long long)a.B * (long long)a.H;
   if (bh > 65535) return fail(DSATTN_EINVAL, "B*H must be <= 65535 (got %lld)", bh);
   if ((long long)a.N * kHeadDim * bh > (1LL << 40))
@@ -119,6 +122,7 @@ int launch_attention(const dsattn_args& a, const Request& rq) {
   p.o = static_cast<uint16_t*>(a.o);
   p.N = a.N;
   p.n_qt = (a.N + kTileQ - 1) / kTileQ;
+  p.n_qu = (a.N + a.tile_q - 1) / a.tile_q;
   p.n_kt = (a.N + kTileK - 1) / kTileK;
   p.c = (float)((double)a.scale * kLog2e);
   p.thr = rq.thr_log2;
@@ -129,7 +133,7 @@ int launch_attention(const dsattn_args& a, const Request& rq) {
   if (p.stats != nullptr &&
       dsattn::launch_zero_u64(p.stats, (int)(bh * 4), a.stream) != hipSuccess)
     return fail(DSATTN_ELAUNCH, "zero-fill launch failed");
-  const hipError_t e = dsattn::launch_fa_fwd(rq.rule, p, (int)bh, a.stream);
+  const hipError_t e = dsattn::launch_fa_fwd(rq.rule, a.tile_q, p, (int)bh, a.stream);
   if (e != hipSuccess) return fail(DSATTN_ELAUNCH, "kernel launch failed: %s", hipGetErrorString(e));
   return DSATTN_OK;
 }

@@ -304,10 +304,11 @@ struct LoopCtx {
   __amdgpu_buffer_rsrc_t krs;   // K / V of this head as buffer resources
   __amdgpu_buffer_rsrc_t vrs;
   uint32_t koff, voff;          // lane offsets inside a 1 KiB tile block
-  uint8_t* mask_row;
+  uint8_t* mask_row;            // this decision unit's row of the skip mask, or null
   float c;
   float thr;
-  int N, n_kt, w, lane, r, g, rows_valid;
+  int N, n_kt, w, lane, r, g;
+  int rows_valid;               // valid query rows of this decision unit
   bool valid, ragged;
 };
 
@@ -316,56 +317,59 @@ struct SkipCount {
   uint64_t elems = 0;
 };
 
-// One key tile j.  On entry s_cur holds S_j, mhat its row max (log2 units), keep the
-// workgroup's decision for tile j, and v_ready says whether V_j is already in LDS
-// (buffer j % 2).  On exit s_next holds S_{j+1}, mhat / keep / v_ready refer to tile j+1,
-// and every wave has passed the barrier that publishes K_{j+2}, the V_{j+1} buffer if it
-// was requested, and the tile-(j+1) votes.
+// One key tile j.  On entry s_cur holds S_j, mhat its row max (log2 units), keep_own
+// the decision for tile j of this wave's decision unit (the workgroup's 128 query rows,
+// or with UNIT = 32 the wave's own rows), keep_any whether any unit of the workgroup keeps
+// tile j, and v_ready whether V_j is already in LDS (buffer j % 2).  On exit s_next holds
+// S_{j+1}, the other state refers to tile j+1, and every wave has passed the barrier that
+// publishes K_{j+2}, the V_{j+1} buffer if it was requested, and the tile-(j+1) votes.
 //
-// V tiles are fetched for kept tiles only.  V_{j+1} is requested one iteration ahead when
-// tile j is kept (runs of kept tiles are the common case); after a skipped tile, a kept
-// tile's V is requested at the start of its own iteration, so a run of skipped tiles
-// streams K alone.
-template <int RULE>
+// V tiles are fetched for tiles some unit keeps.  V_{j+1} is requested one iteration
+// ahead when tile j is kept (runs of kept tiles are the common case); after a skipped
+// tile, a kept tile's V is requested at the start of its own iteration, so a run of
+// skipped tiles streams K alone.
+template <int RULE, int UNIT>
 __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f32x16 (&s_next)[2],
-                                              float& mhat, bool& keep, bool& v_ready,
-                                              RowState& rs, f32x16 (&o)[4],
+                                              float& mhat, bool& keep_own, bool& keep_any,
+                                              bool& v_ready, RowState& rs, f32x16 (&o)[4],
                                               const bf16x8 (&qf)[8], Smem& sm,
                                               const LoopCtx& cx, SkipCount& sk) {
   const int nb = (j + 1) & 1;
   const bool has_next = (j + 1) < cx.n_kt;
-  if (cx.mask_row != nullptr && cx.w == 0 && cx.lane == 0) cx.mask_row[j] = keep ? 0 : 1;
+  if (cx.mask_row != nullptr && (UNIT == kTQ ? cx.w == 0 : true) && cx.lane == 0)
+    cx.mask_row[j] = keep_own ? 0 : 1;
 
   // Tile loads.  Past the last tile the range check returns zeros into buffers nobody
   // reads.  A kept tile after a skipped one fetches its own V first and waits for it (all
   // waves' shares) before anything else: real masks change between kept and skipped
   // rarely (about one tile in twenty at 30 % sparsity on video inputs), and this keeps
   // the kept-tile code identical to the dense kernel's.
-  const bool late_v = keep && !v_ready;
+  const bool late_v = keep_any && !v_ready;
   if (late_v) {
     load_tile_lds(sm.v[j & 1], cx.vrs, cx.voff, j * kTK, cx.w);
     asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
   }
-  if (keep) load_tile_lds(sm.v[nb], cx.vrs, cx.voff, (j + 1) * kTK, cx.w);
+  if (keep_any) load_tile_lds(sm.v[nb], cx.vrs, cx.voff, (j + 1) * kTK, cx.w);
   load_tile_lds(sm.k[j & 1], cx.krs, cx.koff, (j + 2) * kTK, cx.w);
 
   // S_{j+1} is computed on both paths (on the last tile it reads a stale buffer and is
   // dropped).
-  if (keep) {
+  if (keep_own) {
     kept_tile(rs, o, s_cur, mhat, cx.c, s_next, sm.k[nb], sm.v[j & 1], qf, cx.r, cx.g, cx.lane);
   } else {
     sk.tiles += 1;
     sk.elems += (uint64_t)cx.rows_valid * (uint64_t)min(kTK, cx.N - j * kTK);
     skipped_tile(s_next, sm.k[nb], qf, cx.r, cx.g);
   }
-  v_ready = keep;
+  v_ready = keep_any;
 
   float mhat_next = 0.f;
+  bool wave_keeps = true;
   if (has_next) {
     if (cx.ragged && j + 2 == cx.n_kt) mask_tail(s_next, (j + 1) * kTK, cx.N, cx.g);
     mhat_next = row_max(s_next) * cx.c;
     if constexpr (RULE != kRuleDense) {
-      const bool wave_keeps = __ballot(cx.valid & row_keeps<RULE>(rs, mhat_next, cx.thr)) != 0;
+      wave_keeps = __ballot(cx.valid & row_keeps<RULE>(rs, mhat_next, cx.thr)) != 0;
       if (cx.lane == 0) sm.vote[nb][cx.w] = wave_keeps ? 1 : 0;
     }
   }
@@ -374,16 +378,21 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
   // drain every load again on its own.)
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
   if (has_next) {
-    if constexpr (RULE != kRuleDense)
-      keep = __builtin_amdgcn_readfirstlane(*reinterpret_cast<const uint32_t*>(sm.vote[nb])) != 0;
+    if constexpr (RULE != kRuleDense) {
+      keep_any = __builtin_amdgcn_readfirstlane(
+                     *reinterpret_cast<const uint32_t*>(sm.vote[nb])) != 0;
+      keep_own = UNIT == kTQ ? keep_any : wave_keeps;
+    }
     mhat = mhat_next;
   }
 }
 
-template <int RULE>
+// UNIT: query rows per skip decision, 128 (the workgroup's tile) or 32 (one wave).
+template <int RULE, int UNIT>
 __global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads),
                           amdgpu_waves_per_eu(2, 2))) void
 fa_fwd_kernel(FwdParams p) {
+  static_assert(UNIT == kTQ || UNIT == 32, "decision unit is the tile or one wave");
   __shared__ __attribute__((aligned(16))) Smem sm;
 
   const int tid = threadIdx.x;
@@ -398,7 +407,6 @@ fa_fwd_kernel(FwdParams p) {
                                              0x00020000);
   cx.vrs = __builtin_amdgcn_make_buffer_rsrc((void*)(p.v + head_off), (short)0, head_bytes,
                                              0x00020000);
-  cx.mask_row = p.mask != nullptr ? p.mask + ((size_t)bh * p.n_qt + qt) * p.n_kt : nullptr;
   cx.c = p.c;
   cx.thr = p.thr;
   cx.N = N;
@@ -412,8 +420,14 @@ fa_fwd_kernel(FwdParams p) {
   const int q0 = qt * kTQ;
   const int qrow = q0 + cx.w * 32 + cx.r;
   cx.valid = qrow < N;
-  cx.rows_valid = min(kTQ, N - q0);
   cx.ragged = (N % kTK) != 0;
+  // This wave's decision unit: the workgroup's tile, or the wave's own 32 rows.
+  const int unit = UNIT == kTQ ? qt : qt * (kTQ / UNIT) + cx.w;
+  const int unit_row0 = unit * UNIT;
+  cx.rows_valid = max(0, min(UNIT, N - unit_row0));
+  cx.mask_row = (p.mask != nullptr && cx.rows_valid > 0)
+                    ? p.mask + ((size_t)bh * p.n_qu + unit) * p.n_kt
+                    : nullptr;
 
   // Stage K_0 and V_0, then K_1.
   load_tile_lds(sm.k[0], cx.krs, cx.koff, 0, cx.w);
@@ -441,16 +455,19 @@ fa_fwd_kernel(FwdParams p) {
   skipped_tile(sa, sm.k[0], qf, cx.r, cx.g);   // S_0
   if (cx.ragged && cx.n_kt == 1) mask_tail(sa, 0, N, cx.g);
   float mhat = row_max(sa) * cx.c;
-  bool keep = true;                          // the first tile is always kept
+  bool keep_own = true;                      // the first tile is always kept
+  bool keep_any = true;
   bool v_ready = true;                       // V_0 was staged above
   SkipCount sk;
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");  // K_0 consumed
 
   // Unrolled by two so that S_j / S_{j+1} alternate between sa and sb without copies.
   for (int j = 0; j < cx.n_kt; j += 2) {
-    key_tile_step<RULE>(j, sa, sb, mhat, keep, v_ready, rs, o, qf, sm, cx, sk);
+    key_tile_step<RULE, UNIT>(j, sa, sb, mhat, keep_own, keep_any, v_ready, rs, o, qf, sm, cx,
+                              sk);
     if (j + 1 < cx.n_kt)
-      key_tile_step<RULE>(j + 1, sb, sa, mhat, keep, v_ready, rs, o, qf, sm, cx, sk);
+      key_tile_step<RULE, UNIT>(j + 1, sb, sa, mhat, keep_own, keep_any, v_ready, rs, o, qf,
+                                sm, cx, sk);
   }
 
   // ---- epilogue: renormalise over kept keys, store O (bf16) and the row LSE --------
@@ -471,7 +488,9 @@ fa_fwd_kernel(FwdParams p) {
     if (p.lse != nullptr && cx.g == 0)
       p.lse[(size_t)bh * N + qrow] = (rs.m_ref + log2_fast(l_row)) * 0.69314718055994530942f;
   }
-  if (p.stats != nullptr && tid == 0) {
+  // One set of counters per decision unit (the workgroup's tile, or each wave's rows).
+  if (p.stats != nullptr && (UNIT == kTQ ? cx.w == 0 : true) && cx.lane == 0 &&
+      cx.rows_valid > 0) {
     unsigned long long* st = reinterpret_cast<unsigned long long*>(p.stats) + (size_t)bh * 4;
     atomicAdd(st + 0, (unsigned long long)cx.n_kt);
     atomicAdd(st + 1, (unsigned long long)sk.tiles);
@@ -487,23 +506,35 @@ __global__ void zero_u64_kernel(uint64_t* __restrict__ p, int n) {
 
 }  // namespace
 
-hipError_t launch_fa_fwd(int rule, const FwdParams& p, int bh, hipStream_t stream) {
-  const dim3 grid((unsigned)p.n_qt, (unsigned)bh);
+namespace {
+
+template <int UNIT>
+hipError_t launch_unit(int rule, const FwdParams& p, dim3 grid, hipStream_t stream) {
   const dim3 block(kThreads);
   switch (rule) {
     case kRuleDense:
-      hipLaunchKernelGGL(fa_fwd_kernel<kRuleDense>, grid, block, 0, stream, p);
+      hipLaunchKernelGGL((fa_fwd_kernel<kRuleDense, UNIT>), grid, block, 0, stream, p);
       break;
     case kRuleBlasst:
-      hipLaunchKernelGGL(fa_fwd_kernel<kRuleBlasst>, grid, block, 0, stream, p);
+      hipLaunchKernelGGL((fa_fwd_kernel<kRuleBlasst, UNIT>), grid, block, 0, stream, p);
       break;
     case kRuleDynSparse:
-      hipLaunchKernelGGL(fa_fwd_kernel<kRuleDynSparse>, grid, block, 0, stream, p);
+      hipLaunchKernelGGL((fa_fwd_kernel<kRuleDynSparse, UNIT>), grid, block, 0, stream, p);
       break;
     default:
       return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_fa_fwd(int rule, int unit_rows, const FwdParams& p, int bh,
+                         hipStream_t stream) {
+  const dim3 grid((unsigned)p.n_qt, (unsigned)bh);
+  if (unit_rows == kTQ) return launch_unit<kTQ>(rule, p, grid, stream);
+  if (unit_rows == 32) return launch_unit<32>(rule, p, grid, stream);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_zero_u64(uint64_t* ptr, int n, hipStream_t stream) {

@@ -15,17 +15,20 @@ struct FwdParams {
   const uint16_t* v;
   uint16_t* o;
   int N;
-  int n_qt;            // ceil(N / 128)
+  int n_qt;            // ceil(N / 128): query tiles (workgroups per head)
+  int n_qu;            // ceil(N / unit rows): skip-decision units per head (mask rows)
   int n_kt;            // ceil(N / 64)
   float c;             // scale * log2(e): logits are handled in log2 units
   float thr;           // skip threshold in log2 units (lambda*log2(e) or log2(tau))
   uint64_t* stats;     // [BH][4] or null (zeroed beforehand)
-  uint8_t* mask;       // [BH][n_qt][n_kt] or null
+  uint8_t* mask;       // [BH][n_qu][n_kt] or null
   float* lse;          // [BH][N] or null
 };
 
-// Enqueue one forward pass over `bh` heads on `stream`.
-hipError_t launch_fa_fwd(int rule, const FwdParams& p, int bh, hipStream_t stream);
+// Enqueue one forward pass over `bh` heads on `stream`; unit_rows (128 or 32) is the
+// number of query rows that share one skip decision.
+hipError_t launch_fa_fwd(int rule, int unit_rows, const FwdParams& p, int bh,
+                         hipStream_t stream);
 
 // Enqueue a fill of n uint64 zeros (a kernel rather than a memset node, so the call can be
 // captured into a graph and replayed).

@@ -103,6 +103,8 @@ def _fwd(name, param, B=1, H=1, N=128, d=128, scale=0.1, tq=128, tk=64, ptr=None
     ("blasst_attn_fwd", 1.1, {}, -1, "tau"),
     ("dynsparse_attn_fwd", 0.95, {"d": 64}, -2, "head dimension"),
     ("dynsparse_attn_fwd", 0.95, {"tq": 64}, -2, "tile"),
+    ("dynsparse_attn_fwd", 0.95, {"tq": 32, "tk": 32}, -2, "tile"),
+    ("dynsparse_attn_fwd", 0.95, {"tq": 32}, -1, "non-null"),   # 32 x 64 passes the shape check
     ("dynsparse_attn_fwd", 0.95, {"tk": 128}, -2, "tile"),
     ("dynsparse_attn_fwd", 0.95, {"N": -1}, -1, ">= 0"),
     ("dynsparse_attn_fwd", 0.95, {"B": -2}, -1, ">= 0"),
@@ -120,7 +122,7 @@ def test_dense_entry_rejects_null_and_bad_tiles():
     rc, err = _call_raw("dense_attn_fwd", None, None, None, None, 1, 1, 16, 128, 0.1, 128, 64,
                         None, None)
     assert rc == -1 and "non-null" in err
-    rc, err = _call_raw("dense_attn_fwd", None, None, None, None, 1, 1, 16, 128, 0.1, 32, 64,
+    rc, err = _call_raw("dense_attn_fwd", None, None, None, None, 1, 1, 16, 128, 0.1, 64, 64,
                         None, None)
     assert rc == -2
 
