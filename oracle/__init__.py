@@ -10,6 +10,7 @@ from .attention import (
     RuleRun,
     bf16_to_f64,
     dense_attention,
+    diagonal_first_order,
     filter_q_tile,
     lambda_from_recall,
     log_threshold_blasst,
@@ -22,6 +23,7 @@ __all__ = [
     "RuleRun",
     "bf16_to_f64",
     "dense_attention",
+    "diagonal_first_order",
     "filter_q_tile",
     "lambda_from_recall",
     "log_threshold_blasst",

@@ -106,26 +106,31 @@ class QTileResult:
 
 
 def filter_q_tile(s: np.ndarray, v: np.ndarray, rule: str, threshold: float, tile_k: int,
-                  forced_skip=None) -> QTileResult:
+                  forced_skip=None, order=None) -> QTileResult:
     """Run the tile loop for one query tile.
 
     ``s``: float64 [rows, N] scaled logits of the tile's valid rows; ``v``: float64 [N, d].
     ``threshold``: lambda (DynSparse) or ln(tau) (BLASST), natural-log units; ignored for
     dense.  ``forced_skip`` (bool [T_c]) makes the loop take those decisions instead of its
     own while still recording its own margins (used to compare against another run's
-    decisions without letting one near-tie change every later decision).
+    decisions without letting one near-tie change every later decision).  ``order``: the
+    sequence in which key tiles are visited (default ascending); the running LSE and max
+    cover the tiles kept earlier in that sequence.  Results are indexed by key tile.
     """
     if rule not in RULES:
         raise ValueError(f"unknown rule {rule!r}")
     rows, n = s.shape
     n_kt = -(-n // tile_k)
+    order = list(range(n_kt)) if order is None else [int(j) for j in order]
+    if sorted(order) != list(range(n_kt)):
+        raise ValueError("order must visit every key tile exactly once")
     lse = np.full(rows, -np.inf)      # LSE over kept tiles so far (Eq. 6)
     m_run = np.full(rows, -np.inf)    # running max over kept tiles
     skip = np.zeros(n_kt, dtype=bool)
     margin = np.zeros(n_kt)
     tmetric = np.zeros((rows, n_kt))
     kept = []
-    for j in range(n_kt):
+    for j in order:
         cols = slice(j * tile_k, min(n, (j + 1) * tile_k))
         blk = s[:, cols]
         m_hat = blk.max(axis=1)
@@ -179,14 +184,36 @@ class RuleRun:
         return out
 
 
+def diagonal_first_order(n_kt: int, start: int) -> list:
+    """Key tiles ranked by their distance from ``start``: the start tile, then the tile
+    after it, the tile before it, two after, two before, and so on; once one side runs out
+    the other continues in order.  (A reading of the "diagonal-first" key order: for
+    self-attention the tiles around a query tile's own position come first.)"""
+    if not 0 <= start < n_kt:
+        raise ValueError("start must be a key tile")
+
+    def rank(t):
+        if t == start:
+            return 0
+        return 2 * (t - start) - 1 if t > start else 2 * (start - t)
+
+    return sorted(range(n_kt), key=rank)
+
+
 def rule_attention(q_bits, k_bits, v_bits, scale, rule, threshold, tile_q, tile_k,
-                   tiles=None, forced_mask=None) -> RuleRun:
+                   tiles=None, forced_mask=None, key_order="ascending",
+                   order_rows=128) -> RuleRun:
     """Run the oracle on bf16 inputs ``[B][H][N][d]`` (uint16 bit patterns).
 
     ``tiles``: iterable of (b, h, qi) to evaluate (default: every query tile of every
     head).  ``forced_mask``: optional uint8/bool array [B][H][T_r][T_c] of decisions to
-    follow (see ``filter_q_tile``).
+    follow (see ``filter_q_tile``).  ``key_order``: "ascending" or "diagonal"; the
+    diagonal order of a query tile starts at the key tile holding the first row of the
+    ``order_rows``-row block that contains the query tile (so query tiles smaller than
+    that block share one order).
     """
+    if key_order not in ("ascending", "diagonal"):
+        raise ValueError(f"unknown key order {key_order!r}")
     B, H, N, d = q_bits.shape
     n_qt = -(-N // tile_q)
     if tiles is None:
@@ -203,6 +230,10 @@ def rule_attention(q_bits, k_bits, v_bits, scale, rule, threshold, tile_q, tile_
         q64 = bf16_to_f64(q_bits[b, h, r0:r1])
         s = scale * (q64 @ k64.T)
         forced = None if forced_mask is None else np.asarray(forced_mask[b, h, qi]).astype(bool)
-        results.append(filter_q_tile(s, v64, rule, threshold, tile_k, forced))
+        order = None
+        if key_order == "diagonal":
+            block_row0 = (r0 // order_rows) * order_rows
+            order = diagonal_first_order(-(-N // tile_k), block_row0 // tile_k)
+        results.append(filter_q_tile(s, v64, rule, threshold, tile_k, forced, order))
         ranges.append((r0, r1))
     return RuleRun(tiles, results, ranges, tile_q, tile_k, N)
