@@ -332,29 +332,27 @@ def sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop):
     import torch
 
     B, H, N = w.B, w.H, w.N
-    # 128-row decisions (the default), then the same rule with every wave's 32 rows
-    # deciding on their own (tile_q = 32).
-    points = [("dense", None, TILE_Q)] + \
-             [("dynsparse_recall", r, TILE_Q) for r in (0.90, 0.95, 0.98, 0.99)] + \
-             [("dynsparse_lambda", l, TILE_Q) for l in (-6.0, -8.0, -10.0)] + \
-             [("blasst", t, TILE_Q) for t in (1e-2, 1e-3, 1e-4)] + \
-             [("dynsparse_recall", 0.95, 32), ("dynsparse_lambda", -6.0, 32),
-              ("dynsparse_lambda", -8.0, 32), ("dynsparse_lambda", -10.0, 32),
-              ("blasst", 1e-2, 32)]
+    # 128-row decisions in ascending key order (the default); then every wave's 32 rows
+    # deciding on their own (tile_q = 32); then the diagonal-first key order.
+    asc, diag = dsa.ORDER_ASCENDING, dsa.ORDER_DIAGONAL
+    points = [("dense", 0.0, TILE_Q, asc)] + \
+             [("dynsparse_recall", r, TILE_Q, asc) for r in (0.90, 0.95, 0.98, 0.99)] + \
+             [("dynsparse_lambda", l, TILE_Q, asc) for l in (-6.0, -8.0, -10.0)] + \
+             [("blasst", t, TILE_Q, asc) for t in (1e-2, 1e-3, 1e-4)] + \
+             [("dynsparse_recall", 0.95, 32, asc), ("dynsparse_lambda", -6.0, 32, asc),
+              ("dynsparse_lambda", -8.0, 32, asc), ("dynsparse_lambda", -10.0, 32, asc),
+              ("blasst", 1e-2, 32, asc)] + \
+             [("dynsparse_recall", 0.95, TILE_Q, diag), ("dynsparse_lambda", -6.0, TILE_Q, diag),
+              ("dynsparse_lambda", -8.0, TILE_Q, diag), ("dynsparse_lambda", -10.0, TILE_Q, diag),
+              ("blasst", 1e-2, TILE_Q, diag), ("dynsparse_lambda", -8.0, 32, diag)]
+    rule_ids = {"dense": dsa.RULE_DENSE, "dynsparse_recall": dsa.RULE_DYNSPARSE_RECALL,
+                "dynsparse_lambda": dsa.RULE_DYNSPARSE_LAMBDA, "blasst": dsa.RULE_BLASST}
     dense_ms = None
-    for rule, p, tq in points:
-        if rule == "dense":
-            fn = lambda: dsa.dense_attn_fwd(qd, kd, vd, od, scale=scale, stats_out=stats)
-        elif rule == "dynsparse_recall":
-            fn = lambda: dsa.dynsparse_attn_fwd(qd, kd, vd, o, scale=scale, recall_target=p,
-                                                tile_q=tq, stats_out=stats)
-        elif rule == "dynsparse_lambda":
-            fn = lambda: dsa.dynsparse_attn_fwd_lambda(qd, kd, vd, o, scale=scale, lam=p,
-                                                       tile_q=tq, stats_out=stats)
-        else:
-            fn = lambda: dsa.blasst_attn_fwd(qd, kd, vd, o, scale=scale, threshold=p,
-                                             tile_q=tq, stats_out=stats)
-        print(f"[sweep] {rule} {p} tile_q={tq}", file=sys.stderr, flush=True)
+    for rule, p, tq, order in points:
+        out = od if rule == "dense" else o
+        fn = lambda: dsa.dsattn_attn_fwd_ex(rule_ids[rule], p, qd, kd, vd, out, scale=scale,
+                                            tile_q=tq, stats_out=stats, key_order=order)
+        print(f"[sweep] {rule} {p} tile_q={tq} order={order}", file=sys.stderr, flush=True)
         ms = time_calls(fn, args.steps, args.warmup)
         st = stats.cpu().numpy().reshape(B * H, 4)
         if rule == "dense":
@@ -363,7 +361,8 @@ def sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop):
         else:
             rel = float((o.float() - od.float()).pow(2).sum().sqrt() /
                         od.float().pow(2).sum().sqrt())
-        rec = {"workload": w.name, "rule": rule, "param": p, "tile_q": tq, "ms": ms,
+        rec = {"workload": w.name, "rule": rule, "param": p, "tile_q": tq,
+               "key_order": "diagonal" if order == diag else "ascending", "ms": ms,
                "effective_tflops": dense_flop / (ms * 1e-3) / 1e12,
                "actual_tflops": algorithmic_flops(st) / (ms * 1e-3) / 1e12,
                "sparsity_tiles": float(st[:, 1].sum() / st[:, 0].sum()),

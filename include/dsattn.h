@@ -64,6 +64,11 @@ typedef enum dsattn_status {
   DSATTN_ELAUNCH = -3      /* the HIP runtime refused a launch */
 } dsattn_status;
 
+typedef enum dsattn_key_order {
+  DSATTN_ORDER_ASCENDING = 0,  /* key tiles 0, 1, 2, ... for every query tile */
+  DSATTN_ORDER_DIAGONAL = 1    /* from the query tile's own position outward, see below */
+} dsattn_key_order;
+
 typedef enum dsattn_rule {
   DSATTN_RULE_DENSE = 0,
   DSATTN_RULE_BLASST = 1,            /* param = tau in [0, 1] */
@@ -126,8 +131,18 @@ typedef struct dsattn_args {
   uint64_t* stats_out;   /* may be NULL */
   uint8_t* mask_out;     /* may be NULL */
   float* lse_out;        /* may be NULL */
+  int key_order;         /* dsattn_key_order; the named entry points use ascending */
 } dsattn_args;
 
+/*
+ * Key-tile visit order.  The rule is order dependent (Eq. 5 compares with the LSE of the
+ * tiles kept before), and the paper walks key tiles in ascending order.  With
+ * DSATTN_ORDER_DIAGONAL every 128-row query block starts at the key tile c that holds its
+ * first row (c = 128 i / tile_k for block i), then visits c+1, c-1, c+2, c-2, ... and,
+ * once one side is used up, the rest of the other side in order; query tiles of 32 rows
+ * use the order of their 128-row block.  For self-attention this visits the keys nearest
+ * each query first.  mask_out is indexed by key tile whatever the order.
+ */
 int dsattn_attn_fwd_ex(const dsattn_args* args);
 
 /*

@@ -31,6 +31,9 @@ RULE_BLASST = 1
 RULE_DYNSPARSE_RECALL = 2
 RULE_DYNSPARSE_LAMBDA = 3
 
+ORDER_ASCENDING = 0
+ORDER_DIAGONAL = 1
+
 _lib = None
 
 
@@ -55,6 +58,7 @@ class DsAttnArgs(ctypes.Structure):
         ("stats_out", ctypes.c_void_p),
         ("mask_out", ctypes.c_void_p),
         ("lse_out", ctypes.c_void_p),
+        ("key_order", ctypes.c_int),
     ]
 
 
@@ -227,14 +231,15 @@ def dense_attn_fwd(q, k, v, o=None, scale=None, tile_q=TILE_Q, tile_k=TILE_K,
 
 def dsattn_attn_fwd_ex(rule, param, q, k, v, o=None, scale=None, tile_q=TILE_Q,
                        tile_k=TILE_K, stats_out=None, mask_out=None, lse_out=None,
-                       stream=None):
-    """Any rule (RULE_* constants) with optional stats, skip mask and LSE outputs."""
+                       stream=None, key_order=ORDER_ASCENDING):
+    """Any rule (RULE_* constants) with optional stats, skip mask and LSE outputs, and
+    the key-tile visit order (ORDER_* constants)."""
     o = _out(q, o)
     B, H, N, d = _shape(q, k, v, o)
     scale = 1.0 / math.sqrt(d) if scale is None else scale
     st, mk, ls = _buffers(B, H, N, stats_out, mask_out, lse_out, tile_q)
     a = DsAttnArgs(rule, param, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
-                   B, H, N, d, scale, tile_q, tile_k, _stream(stream), st, mk, ls)
+                   B, H, N, d, scale, tile_q, tile_k, _stream(stream), st, mk, ls, key_order)
     _check(lib().dsattn_attn_fwd_ex(ctypes.byref(a)), "dsattn_attn_fwd_ex")
     return o
 
@@ -297,7 +302,8 @@ def dsattn_reordered_workspace_bytes(B, H, N, d=HEAD_DIM, with_lse=False):
 
 def dsattn_attn_fwd_reordered(rule, param, q, k, v, q_index, kv_index, o=None, scale=None,
                               tile_q=TILE_Q, tile_k=TILE_K, stats_out=None, mask_out=None,
-                              lse_out=None, workspace=None, stream=None):
+                              lse_out=None, workspace=None, stream=None,
+                              key_order=ORDER_ASCENDING):
     """``dsattn_attn_fwd_ex`` over queries taken in ``q_index`` order and keys/values in
     ``kv_index`` order (int32 GPU tensors); o and lse_out come back in the original query
     order, mask_out and stats_out describe the reordered tiles.  ``workspace`` (a uint8
@@ -315,7 +321,7 @@ def dsattn_attn_fwd_reordered(rule, param, q, k, v, q_index, kv_index, o=None, s
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
     a = DsAttnArgs(rule, param, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
-                   B, H, N, d, scale, tile_q, tile_k, _stream(stream), st, mk, ls)
+                   B, H, N, d, scale, tile_q, tile_k, _stream(stream), st, mk, ls, key_order)
     rc = lib().dsattn_attn_fwd_reordered(ctypes.byref(a), q_index.data_ptr(),
                                          kv_index.data_ptr(), workspace.data_ptr(),
                                          workspace.numel() * workspace.element_size())
@@ -324,7 +330,7 @@ def dsattn_attn_fwd_reordered(rule, param, q, k, v, q_index, kv_index, o=None, s
 
 
 __all__ = [
-    "HEAD_DIM", "TILE_Q", "TILE_K", "RULE_DENSE", "RULE_BLASST", "RULE_DYNSPARSE_RECALL",
+    "HEAD_DIM", "TILE_Q", "TILE_K", "ORDER_ASCENDING", "ORDER_DIAGONAL", "RULE_DENSE", "RULE_BLASST", "RULE_DYNSPARSE_RECALL",
     "RULE_DYNSPARSE_LAMBDA", "DsAttnArgs", "lib", "last_error", "dsattn_lambda_from_recall",
     "dynsparse_attn_fwd", "dynsparse_attn_fwd_lambda", "blasst_attn_fwd", "dense_attn_fwd",
     "dsattn_attn_fwd_ex", "dsattn_block_order", "dsattn_gather_rows", "dsattn_scatter_rows",

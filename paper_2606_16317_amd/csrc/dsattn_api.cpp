@@ -69,6 +69,8 @@ int check_problem(const dsattn_args& a) {
   if (bh > 65535) return fail(DSATTN_EINVAL, "B*H must be <= 65535 (got %lld)", bh);
   if ((long long)a.N * kHeadDim * bh > (1LL << 40))
     return fail(DSATTN_EINVAL, "problem too large");
+  if (a.key_order != DSATTN_ORDER_ASCENDING && a.key_order != DSATTN_ORDER_DIAGONAL)
+    return fail(DSATTN_EINVAL, "unknown key order %d", a.key_order);
   return DSATTN_OK;
 }
 
@@ -129,6 +131,8 @@ int launch_attention(const dsattn_args& a, const Request& rq) {
   p.stats = a.stats_out;
   p.mask = a.mask_out;
   p.lse = a.lse_out;
+  p.key_order = a.key_order == DSATTN_ORDER_DIAGONAL ? dsattn::kOrderDiagonal
+                                                     : dsattn::kOrderAscending;
 
   if (p.stats != nullptr &&
       dsattn::launch_zero_u64(p.stats, (int)(bh * 4), a.stream) != hipSuccess)
@@ -261,6 +265,7 @@ dsattn_args make_args(int rule, float param, const void* q, const void* k, const
   a.stats_out = stats_out;
   a.mask_out = nullptr;
   a.lse_out = nullptr;
+  a.key_order = DSATTN_ORDER_ASCENDING;
   return a;
 }
 

@@ -310,14 +310,40 @@ struct LoopCtx {
   int N, n_kt, w, lane, r, g;
   int rows_valid;               // valid query rows of this decision unit
   bool valid, ragged;
+  // Diagonal-first visit order around key tile diag_c (the tile holding the workgroup's
+  // first query row): diag_c, diag_c + 1, diag_c - 1, ..., then on along the longer side
+  // once the shorter one (diag_m tiles) is used up.
+  bool diag_right;
+  int diag_c, diag_m;
 };
+
+// Key tile visited at loop step s (0 <= s < n_kt) in order ORDER.
+template <int ORDER>
+__device__ __forceinline__ int key_tile_at(int s, const LoopCtx& cx) {
+  if constexpr (ORDER == kOrderAscending) {
+    return s;
+  } else {
+    if (s <= 2 * cx.diag_m) return (s & 1) ? cx.diag_c + ((s + 1) >> 1) : cx.diag_c - (s >> 1);
+    const int t = s - 2 * cx.diag_m;
+    return cx.diag_right ? cx.diag_c + cx.diag_m + t : cx.diag_c - cx.diag_m - t;
+  }
+}
+
+// Key tile of step s, or the first tile past the sequence for steps beyond the loop (its
+// loads come back as zeros and are never read).
+template <int ORDER>
+__device__ __forceinline__ int key_tile_or_past(int s, const LoopCtx& cx) {
+  if constexpr (ORDER == kOrderAscending) return s;   // already past the end when s >= n_kt
+  return s < cx.n_kt ? key_tile_at<ORDER>(s, cx) : cx.n_kt;
+}
 
 struct SkipCount {
   uint32_t tiles = 0;
   uint64_t elems = 0;
 };
 
-// One key tile j.  On entry s_cur holds S_j, mhat its row max (log2 units), keep_own
+// One loop step j, visiting key tile key_tile_at(j) (written "tile j" below; LDS buffers
+// rotate with the step).  On entry s_cur holds S_j, mhat its row max (log2 units), keep_own
 // the decision for tile j of this wave's decision unit (the workgroup's 128 query rows,
 // or with UNIT = 32 the wave's own rows), keep_any whether any unit of the workgroup keeps
 // tile j, and v_ready whether V_j is already in LDS (buffer j % 2).  On exit s_next holds
@@ -328,7 +354,7 @@ struct SkipCount {
 // ahead when tile j is kept (runs of kept tiles are the common case); after a skipped
 // tile, a kept tile's V is requested at the start of its own iteration, so a run of
 // skipped tiles streams K alone.
-template <int RULE, int UNIT>
+template <int RULE, int UNIT, int ORDER>
 __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f32x16 (&s_next)[2],
                                               float& mhat, bool& keep_own, bool& keep_any,
                                               bool& v_ready, RowState& rs, f32x16 (&o)[4],
@@ -336,8 +362,11 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
                                               const LoopCtx& cx, SkipCount& sk) {
   const int nb = (j + 1) & 1;
   const bool has_next = (j + 1) < cx.n_kt;
+  const int tj = key_tile_at<ORDER>(j, cx);          // key tiles of steps j, j+1, j+2
+  const int tn = key_tile_or_past<ORDER>(j + 1, cx);
+  const int tn2 = key_tile_or_past<ORDER>(j + 2, cx);
   if (cx.mask_row != nullptr && (UNIT == kTQ ? cx.w == 0 : true) && cx.lane == 0)
-    cx.mask_row[j] = keep_own ? 0 : 1;
+    cx.mask_row[tj] = keep_own ? 0 : 1;
 
   // Tile loads.  Past the last tile the range check returns zeros into buffers nobody
   // reads.  A kept tile after a skipped one fetches its own V first and waits for it (all
@@ -346,11 +375,11 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
   // the kept-tile code identical to the dense kernel's.
   const bool late_v = keep_any && !v_ready;
   if (late_v) {
-    load_tile_lds(sm.v[j & 1], cx.vrs, cx.voff, j * kTK, cx.w);
+    load_tile_lds(sm.v[j & 1], cx.vrs, cx.voff, tj * kTK, cx.w);
     asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
   }
-  if (keep_any) load_tile_lds(sm.v[nb], cx.vrs, cx.voff, (j + 1) * kTK, cx.w);
-  load_tile_lds(sm.k[j & 1], cx.krs, cx.koff, (j + 2) * kTK, cx.w);
+  if (keep_any) load_tile_lds(sm.v[nb], cx.vrs, cx.voff, tn * kTK, cx.w);
+  load_tile_lds(sm.k[j & 1], cx.krs, cx.koff, tn2 * kTK, cx.w);
 
   // S_{j+1} is computed on both paths (on the last tile it reads a stale buffer and is
   // dropped).
@@ -358,7 +387,7 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
     kept_tile(rs, o, s_cur, mhat, cx.c, s_next, sm.k[nb], sm.v[j & 1], qf, cx.r, cx.g, cx.lane);
   } else {
     sk.tiles += 1;
-    sk.elems += (uint64_t)cx.rows_valid * (uint64_t)min(kTK, cx.N - j * kTK);
+    sk.elems += (uint64_t)cx.rows_valid * (uint64_t)min(kTK, cx.N - tj * kTK);
     skipped_tile(s_next, sm.k[nb], qf, cx.r, cx.g);
   }
   v_ready = keep_any;
@@ -366,7 +395,7 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
   float mhat_next = 0.f;
   bool wave_keeps = true;
   if (has_next) {
-    if (cx.ragged && j + 2 == cx.n_kt) mask_tail(s_next, (j + 1) * kTK, cx.N, cx.g);
+    if (cx.ragged && tn == cx.n_kt - 1) mask_tail(s_next, tn * kTK, cx.N, cx.g);
     mhat_next = row_max(s_next) * cx.c;
     if constexpr (RULE != kRuleDense) {
       wave_keeps = __ballot(cx.valid & row_keeps<RULE>(rs, mhat_next, cx.thr)) != 0;
@@ -388,7 +417,8 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
 }
 
 // UNIT: query rows per skip decision, 128 (the workgroup's tile) or 32 (one wave).
-template <int RULE, int UNIT>
+// ORDER: key-tile visit order (ascending or diagonal-first).
+template <int RULE, int UNIT, int ORDER>
 __global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads),
                           amdgpu_waves_per_eu(2, 2))) void
 fa_fwd_kernel(FwdParams p) {
@@ -428,10 +458,14 @@ fa_fwd_kernel(FwdParams p) {
   cx.mask_row = (p.mask != nullptr && cx.rows_valid > 0)
                     ? p.mask + ((size_t)bh * p.n_qu + unit) * p.n_kt
                     : nullptr;
+  cx.diag_c = q0 / kTK;                               // < n_kt since q0 < N
+  cx.diag_m = min(cx.diag_c, cx.n_kt - 1 - cx.diag_c);
+  cx.diag_right = (cx.n_kt - 1 - cx.diag_c) > cx.diag_c;
 
-  // Stage K_0 and V_0, then K_1.
-  load_tile_lds(sm.k[0], cx.krs, cx.koff, 0, cx.w);
-  load_tile_lds(sm.v[0], cx.vrs, cx.voff, 0, cx.w);
+  // Stage K and V of the first visited tile, then K of the second.
+  const int t0 = key_tile_at<ORDER>(0, cx);
+  load_tile_lds(sm.k[0], cx.krs, cx.koff, t0 * kTK, cx.w);
+  load_tile_lds(sm.v[0], cx.vrs, cx.voff, t0 * kTK, cx.w);
 
   // Q^T B-operand fragments: d = 16 s + 8 g + (0..7) of this lane's query row.
   const uint16_t* qb = p.q + head_off;
@@ -448,12 +482,12 @@ fa_fwd_kernel(FwdParams p) {
   for (int db = 0; db < 4; ++db) o[db] = f32x16{};
   RowState rs{-__builtin_inff(), -__builtin_inff(), 0.f};
 
-  load_tile_lds(sm.k[1], cx.krs, cx.koff, kTK, cx.w);
+  load_tile_lds(sm.k[1], cx.krs, cx.koff, key_tile_or_past<ORDER>(1, cx) * kTK, cx.w);
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 
   f32x16 sa[2], sb[2];
-  skipped_tile(sa, sm.k[0], qf, cx.r, cx.g);   // S_0
-  if (cx.ragged && cx.n_kt == 1) mask_tail(sa, 0, N, cx.g);
+  skipped_tile(sa, sm.k[0], qf, cx.r, cx.g);   // S of the first visited tile
+  if (cx.ragged && t0 == cx.n_kt - 1) mask_tail(sa, t0 * kTK, N, cx.g);
   float mhat = row_max(sa) * cx.c;
   bool keep_own = true;                      // the first tile is always kept
   bool keep_any = true;
@@ -463,11 +497,11 @@ fa_fwd_kernel(FwdParams p) {
 
   // Unrolled by two so that S_j / S_{j+1} alternate between sa and sb without copies.
   for (int j = 0; j < cx.n_kt; j += 2) {
-    key_tile_step<RULE, UNIT>(j, sa, sb, mhat, keep_own, keep_any, v_ready, rs, o, qf, sm, cx,
-                              sk);
+    key_tile_step<RULE, UNIT, ORDER>(j, sa, sb, mhat, keep_own, keep_any, v_ready, rs, o, qf,
+                                     sm, cx, sk);
     if (j + 1 < cx.n_kt)
-      key_tile_step<RULE, UNIT>(j + 1, sb, sa, mhat, keep_own, keep_any, v_ready, rs, o, qf,
-                                sm, cx, sk);
+      key_tile_step<RULE, UNIT, ORDER>(j + 1, sb, sa, mhat, keep_own, keep_any, v_ready, rs, o,
+                                       qf, sm, cx, sk);
   }
 
   // ---- epilogue: renormalise over kept keys, store O (bf16) and the row LSE --------
@@ -508,18 +542,22 @@ __global__ void zero_u64_kernel(uint64_t* __restrict__ p, int n) {
 
 namespace {
 
-template <int UNIT>
+template <int UNIT, int ORDER>
 hipError_t launch_unit(int rule, const FwdParams& p, dim3 grid, hipStream_t stream) {
   const dim3 block(kThreads);
   switch (rule) {
     case kRuleDense:
-      hipLaunchKernelGGL((fa_fwd_kernel<kRuleDense, UNIT>), grid, block, 0, stream, p);
+      // Every tile is kept, so the visit order changes nothing but the rounding of the
+      // sums: the dense kernel always walks ascending.
+      hipLaunchKernelGGL((fa_fwd_kernel<kRuleDense, UNIT, kOrderAscending>), grid, block, 0,
+                         stream, p);
       break;
     case kRuleBlasst:
-      hipLaunchKernelGGL((fa_fwd_kernel<kRuleBlasst, UNIT>), grid, block, 0, stream, p);
+      hipLaunchKernelGGL((fa_fwd_kernel<kRuleBlasst, UNIT, ORDER>), grid, block, 0, stream, p);
       break;
     case kRuleDynSparse:
-      hipLaunchKernelGGL((fa_fwd_kernel<kRuleDynSparse, UNIT>), grid, block, 0, stream, p);
+      hipLaunchKernelGGL((fa_fwd_kernel<kRuleDynSparse, UNIT, ORDER>), grid, block, 0, stream,
+                         p);
       break;
     default:
       return hipErrorInvalidValue;
@@ -527,13 +565,19 @@ hipError_t launch_unit(int rule, const FwdParams& p, dim3 grid, hipStream_t stre
   return hipGetLastError();
 }
 
+template <int UNIT>
+hipError_t launch_order(int rule, const FwdParams& p, dim3 grid, hipStream_t stream) {
+  if (p.key_order == kOrderDiagonal) return launch_unit<UNIT, kOrderDiagonal>(rule, p, grid, stream);
+  return launch_unit<UNIT, kOrderAscending>(rule, p, grid, stream);
+}
+
 }  // namespace
 
 hipError_t launch_fa_fwd(int rule, int unit_rows, const FwdParams& p, int bh,
                          hipStream_t stream) {
   const dim3 grid((unsigned)p.n_qt, (unsigned)bh);
-  if (unit_rows == kTQ) return launch_unit<kTQ>(rule, p, grid, stream);
-  if (unit_rows == 32) return launch_unit<32>(rule, p, grid, stream);
+  if (unit_rows == kTQ) return launch_order<kTQ>(rule, p, grid, stream);
+  if (unit_rows == 32) return launch_order<32>(rule, p, grid, stream);
   return hipErrorInvalidValue;
 }
 

@@ -8,6 +8,7 @@
 namespace dsattn {
 
 enum { kRuleDense = 0, kRuleBlasst = 1, kRuleDynSparse = 2 };
+enum { kOrderAscending = 0, kOrderDiagonal = 1 };
 
 struct FwdParams {
   const uint16_t* q;   // bf16 [BH][N][128]
@@ -23,6 +24,7 @@ struct FwdParams {
   uint64_t* stats;     // [BH][4] or null (zeroed beforehand)
   uint8_t* mask;       // [BH][n_qu][n_kt] or null
   float* lse;          // [BH][N] or null
+  int key_order;       // kOrderAscending or kOrderDiagonal
 };
 
 // Enqueue one forward pass over `bh` heads on `stream`; unit_rows (128 or 32) is the

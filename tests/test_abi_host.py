@@ -146,6 +146,18 @@ def test_ex_rejects_unknown_rule_and_null_args():
     assert "unknown rule" in pkg.last_error()
 
 
+def test_ex_rejects_unknown_key_order():
+    pkg = _lib()
+    L = pkg.lib()
+    a = pkg.DsAttnArgs(pkg.RULE_DENSE, 0.0, None, None, None, None, 1, 1, 16, 128, 0.1, 128,
+                       64, None, None, None, None, 7)
+    assert L.dsattn_attn_fwd_ex(ctypes.byref(a)) == -1
+    assert "key order" in pkg.last_error()
+    a.key_order = pkg.ORDER_DIAGONAL
+    assert L.dsattn_attn_fwd_ex(ctypes.byref(a)) == -1
+    assert "non-null" in pkg.last_error()     # a valid order passes to the pointer checks
+
+
 def test_empty_problem_is_a_no_op():
     rc, err = _fwd("dynsparse_attn_fwd", 0.95, N=0)
     assert rc == 0 and err == ""
