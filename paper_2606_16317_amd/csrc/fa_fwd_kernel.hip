@@ -58,6 +58,7 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 constexpr int kD = 128;        // head dimension
 constexpr int kTQ = 128;       // query rows per workgroup (decision granularity)
 constexpr int kTK = 64;        // keys per tile
+constexpr int kXcds = 8;       // accelerator dies; workgroups are dealt to them round-robin
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
 constexpr int kTileElems = kTK * kD;         // 8192 bf16 = 16 KiB
@@ -426,7 +427,18 @@ fa_fwd_kernel(FwdParams p) {
   __shared__ __attribute__((aligned(16))) Smem sm;
 
   const int tid = threadIdx.x;
-  const int qt = blockIdx.x;
+  // Query tile of this workgroup.  In ascending order every workgroup of a head streams
+  // K/V from tile 0 on, so neighbours in dispatch order share tiles in L2 whatever query
+  // tile they hold.  In diagonal-first order each query tile starts at its own position;
+  // there the grid is padded to kXcds chunks of consecutive query tiles and x % kXcds (the
+  // XCD the workgroup lands on) picks the chunk, so the workgroups sharing one XCD's L2
+  // start close together and their outward walks overlap.  Padding workgroups exit here.
+  int qt = blockIdx.x;
+  if constexpr (ORDER == kOrderDiagonal) {
+    const int chunk = (p.n_qt + kXcds - 1) / kXcds;
+    qt = (int)(blockIdx.x % kXcds) * chunk + (int)(blockIdx.x / kXcds);
+    if (qt >= p.n_qt) return;
+  }
   const int bh = blockIdx.y;
   const int N = p.N;
   const size_t head_off = (size_t)bh * (size_t)N * kD;
@@ -567,7 +579,11 @@ hipError_t launch_unit(int rule, const FwdParams& p, dim3 grid, hipStream_t stre
 
 template <int UNIT>
 hipError_t launch_order(int rule, const FwdParams& p, dim3 grid, hipStream_t stream) {
-  if (p.key_order == kOrderDiagonal) return launch_unit<UNIT, kOrderDiagonal>(rule, p, grid, stream);
+  if (p.key_order == kOrderDiagonal && rule != kRuleDense) {
+    const int chunk = (p.n_qt + kXcds - 1) / kXcds;
+    return launch_unit<UNIT, kOrderDiagonal>(rule, p, dim3((unsigned)(chunk * kXcds), grid.y),
+                                             stream);
+  }
   return launch_unit<UNIT, kOrderAscending>(rule, p, grid, stream);
 }
 
