@@ -13,7 +13,9 @@ same layer as a reference point.  One JSON line is printed.
 ``--sweep`` instead prints one JSON line per rule/threshold on the given workload;
 ``--reorder-sweep`` prints, per rule/threshold, the row-major run next to the same run over
 the spatio-temporally blocked token order (``dsattn_attn_fwd_reordered``, gathers and the
-output scatter included in its time), plus the HBM rate of the row gather kernel.
+output scatter included in its time), plus the HBM rate of the row gather kernel;
+``--reuse-sweep`` times a DynSparse call that writes its skip mask, then the mask-reuse call
+(DSATTN_RULE_MASK) that applies that mask, per threshold and decision unit.
 """
 
 from __future__ import annotations
@@ -48,6 +50,8 @@ def parse():
     ap.add_argument("--sweep", action="store_true", help="one line per rule/threshold")
     ap.add_argument("--reorder-sweep", action="store_true",
                     help="row-major vs blocked token order, one line per rule/threshold")
+    ap.add_argument("--reuse-sweep", action="store_true",
+                    help="rule call writing its mask, then mask reuse, one line per threshold")
     ap.add_argument("--q-block", default="2,8,8", help="query block (t,y,x) for --reorder-sweep")
     ap.add_argument("--kv-block", default="1,8,8", help="key/value block for --reorder-sweep")
     ap.add_argument("--calib-copy", action="store_true",
@@ -88,11 +92,12 @@ def time_calls(fn, steps, warmup):
     return start.elapsed_time(end) / steps
 
 
-def algorithmic_flops(stats, d=D):
-    """QK^T on every pair plus P.V on kept pairs: 2*d per valid element each."""
+def algorithmic_flops(stats, d=D, reuse=False):
+    """QK^T on every pair plus P.V on kept pairs: 2*d per valid element each.  A reused
+    mask skips QK^T of the skipped pairs too (reuse=True)."""
     elems = int(stats[:, 2].sum())
     skipped = int(stats[:, 3].sum())
-    return 2 * d * elems + 2 * d * (elems - skipped)
+    return 2 * d * (elems - skipped if reuse else elems) + 2 * d * (elems - skipped)
 
 
 def kernel_source_digest():
@@ -252,6 +257,8 @@ def main():
         return sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop)
     if args.reorder_sweep:
         return reorder_sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop)
+    if args.reuse_sweep:
+        return reuse_sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop)
 
     def step():
         dsa.dynsparse_attn_fwd(qd, kd, vd, o, scale=scale, recall_target=recall, stats_out=stats)
@@ -419,6 +426,37 @@ def reorder_sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop):
                           "sparsity_tiles": float(st[:, 1].sum() / st[:, 0].sum()),
                           "speedup_vs_dense": dense_ms / ms, "rel_l2_vs_dense": rel}
         print(json.dumps(rec), flush=True)
+
+
+def reuse_sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop):
+    import torch
+
+    B, H, N = w.B, w.H, w.N
+    dense_ms = time_calls(lambda: dsa.dense_attn_fwd(qd, kd, vd, od, scale=scale),
+                          args.steps, args.warmup)
+    for tq in (TILE_Q, 32):
+        n_qu, n_kt = -(-N // tq), -(-N // TILE_K)
+        for lam in (-6.0, -8.0, -10.0):
+            mask = torch.zeros(B * H * n_qu * n_kt, dtype=torch.uint8, device="cuda")
+            print(f"[reuse-sweep] lambda={lam} tile_q={tq}", file=sys.stderr, flush=True)
+            rule_ms = time_calls(lambda: dsa.dsattn_attn_fwd_ex(
+                dsa.RULE_DYNSPARSE_LAMBDA, lam, qd, kd, vd, o, scale=scale, tile_q=tq,
+                mask_out=mask), args.steps, args.warmup)
+            sp = float(mask.float().mean())
+            reuse_ms = time_calls(lambda: dsa.dsattn_attn_fwd_ex(
+                dsa.RULE_MASK, 0.0, qd, kd, vd, o, scale=scale, tile_q=tq, mask_in=mask,
+                stats_out=stats), args.steps, args.warmup)
+            st = stats.cpu().numpy().reshape(B * H, 4)
+            rel = float((o.float() - od.float()).pow(2).sum().sqrt() /
+                        od.float().pow(2).sum().sqrt())
+            print(json.dumps({"workload": w.name, "lambda": lam, "tile_q": tq,
+                              "sparsity_tiles": sp, "dense_ms": dense_ms, "rule_ms": rule_ms,
+                              "reuse_ms": reuse_ms,
+                              "reuse_effective_tflops": dense_flop / (reuse_ms * 1e-3) / 1e12,
+                              "reuse_actual_tflops": algorithmic_flops(st, reuse=True) /
+                              (reuse_ms * 1e-3) / 1e12,
+                              "reuse_speedup_vs_dense": dense_ms / reuse_ms,
+                              "rel_l2_vs_dense": rel}), flush=True)
 
 
 if __name__ == "__main__":

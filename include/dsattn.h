@@ -73,7 +73,8 @@ typedef enum dsattn_rule {
   DSATTN_RULE_DENSE = 0,
   DSATTN_RULE_BLASST = 1,            /* param = tau in [0, 1] */
   DSATTN_RULE_DYNSPARSE_RECALL = 2,  /* param = recall target in (0, 1] */
-  DSATTN_RULE_DYNSPARSE_LAMBDA = 3   /* param = lambda (finite, or -inf for dense) */
+  DSATTN_RULE_DYNSPARSE_LAMBDA = 3,  /* param = lambda (finite, or -inf for dense) */
+  DSATTN_RULE_MASK = 4               /* reuse a skip mask: args->mask_in; param unused */
 } dsattn_rule;
 
 /*
@@ -132,6 +133,7 @@ typedef struct dsattn_args {
   uint8_t* mask_out;     /* may be NULL */
   float* lse_out;        /* may be NULL */
   int key_order;         /* dsattn_key_order; the named entry points use ascending */
+  const uint8_t* mask_in; /* DSATTN_RULE_MASK only, else ignored (see below) */
 } dsattn_args;
 
 /*
@@ -144,6 +146,20 @@ typedef struct dsattn_args {
  * each query first.  mask_out is indexed by key tile whatever the order.
  */
 int dsattn_attn_fwd_ex(const dsattn_args* args);
+
+/*
+ * Mask reuse (DSATTN_RULE_MASK).  The skip decisions of an earlier call -- typically the
+ * same layer at an earlier denoising step, whose attention changes slowly (the reuse the
+ * paper cites from LiteAttention in Section 1) -- are applied as given: mask_in is a
+ * device uint8 array laid out like mask_out ([B*H][ceil(N/tile_q)][ceil(N/tile_k)],
+ * nonzero = skip), and the output is attention over the kept key tiles, renormalised as
+ * for the rules.  Skipped tiles cost nothing, not even Q K^T: each workgroup visits only
+ * the tiles one of its rows keeps, in ascending order.  A unit that keeps no tile gets
+ * zeros and an LSE of -inf.  Reusing the mask a rule call wrote (same inputs, tile_q and
+ * ascending order) reproduces that call's output bit for bit.  Requirements: mask_in
+ * non-NULL, key_order ascending, ceil(N/tile_k) <= 4096 (N <= 262144), else
+ * DSATTN_EINVAL / DSATTN_EUNSUPPORTED.  mask_out, if given, receives mask_in (as 0/1).
+ */
 
 /*
  * Spatio-temporal token reordering (Section 3.1, closing remark on hyperparameter

@@ -30,6 +30,7 @@ RULE_DENSE = 0
 RULE_BLASST = 1
 RULE_DYNSPARSE_RECALL = 2
 RULE_DYNSPARSE_LAMBDA = 3
+RULE_MASK = 4
 
 ORDER_ASCENDING = 0
 ORDER_DIAGONAL = 1
@@ -59,6 +60,7 @@ class DsAttnArgs(ctypes.Structure):
         ("mask_out", ctypes.c_void_p),
         ("lse_out", ctypes.c_void_p),
         ("key_order", ctypes.c_int),
+        ("mask_in", ctypes.c_void_p),
     ]
 
 
@@ -231,15 +233,23 @@ def dense_attn_fwd(q, k, v, o=None, scale=None, tile_q=TILE_Q, tile_k=TILE_K,
 
 def dsattn_attn_fwd_ex(rule, param, q, k, v, o=None, scale=None, tile_q=TILE_Q,
                        tile_k=TILE_K, stats_out=None, mask_out=None, lse_out=None,
-                       stream=None, key_order=ORDER_ASCENDING):
+                       stream=None, key_order=ORDER_ASCENDING, mask_in=None):
     """Any rule (RULE_* constants) with optional stats, skip mask and LSE outputs, and
-    the key-tile visit order (ORDER_* constants)."""
+    the key-tile visit order (ORDER_* constants).  RULE_MASK reuses ``mask_in`` (a uint8
+    GPU tensor laid out like ``mask_out``)."""
+    import torch
+
     o = _out(q, o)
     B, H, N, d = _shape(q, k, v, o)
     scale = 1.0 / math.sqrt(d) if scale is None else scale
     st, mk, ls = _buffers(B, H, N, stats_out, mask_out, lse_out, tile_q)
+    mi = None
+    if mask_in is not None:
+        n_qu = -(-N // max(1, tile_q))
+        mi = _ptr(mask_in, B * H * n_qu * (-(-N // TILE_K)), (torch.uint8,), "mask_in")
     a = DsAttnArgs(rule, param, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
-                   B, H, N, d, scale, tile_q, tile_k, _stream(stream), st, mk, ls, key_order)
+                   B, H, N, d, scale, tile_q, tile_k, _stream(stream), st, mk, ls, key_order,
+                   mi)
     _check(lib().dsattn_attn_fwd_ex(ctypes.byref(a)), "dsattn_attn_fwd_ex")
     return o
 
@@ -331,7 +341,7 @@ def dsattn_attn_fwd_reordered(rule, param, q, k, v, q_index, kv_index, o=None, s
 
 __all__ = [
     "HEAD_DIM", "TILE_Q", "TILE_K", "ORDER_ASCENDING", "ORDER_DIAGONAL", "RULE_DENSE", "RULE_BLASST", "RULE_DYNSPARSE_RECALL",
-    "RULE_DYNSPARSE_LAMBDA", "DsAttnArgs", "lib", "last_error", "dsattn_lambda_from_recall",
+    "RULE_DYNSPARSE_LAMBDA", "RULE_MASK", "DsAttnArgs", "lib", "last_error", "dsattn_lambda_from_recall",
     "dynsparse_attn_fwd", "dynsparse_attn_fwd_lambda", "blasst_attn_fwd", "dense_attn_fwd",
     "dsattn_attn_fwd_ex", "dsattn_block_order", "dsattn_gather_rows", "dsattn_scatter_rows",
     "dsattn_reordered_workspace_bytes", "dsattn_attn_fwd_reordered",

@@ -22,6 +22,7 @@ constexpr int kHeadDim = 128;
 constexpr int kTileQ = 128;
 constexpr int kTileK = 64;
 constexpr int kUnitWave = 32;  // tile_q = 32: each wave's 32 rows decide on their own
+constexpr int kMaxMaskTiles = 4096;  // key tiles per head the mask-reuse kernel can list
 constexpr double kLog2e = 1.4426950408889634074;
 
 __attribute__((format(printf, 2, 3))) int fail(int code, const char* fmt, ...) {
@@ -71,6 +72,13 @@ int check_problem(const dsattn_args& a) {
     return fail(DSATTN_EINVAL, "problem too large");
   if (a.key_order != DSATTN_ORDER_ASCENDING && a.key_order != DSATTN_ORDER_DIAGONAL)
     return fail(DSATTN_EINVAL, "unknown key order %d", a.key_order);
+  if (a.rule == DSATTN_RULE_MASK) {
+    if (a.key_order != DSATTN_ORDER_ASCENDING)
+      return fail(DSATTN_EUNSUPPORTED, "mask reuse visits key tiles in ascending order only");
+    if ((long long)a.N > (long long)kMaxMaskTiles * kTileK)
+      return fail(DSATTN_EUNSUPPORTED, "mask reuse supports N <= %d (got %d)",
+                  kMaxMaskTiles * kTileK, a.N);
+  }
   return DSATTN_OK;
 }
 
@@ -98,6 +106,11 @@ int check_pointers(const dsattn_args& a) {
     return fail(DSATTN_EINVAL, "lse_out is not a device pointer");
   if (a.lse_out != nullptr && !aligned(a.lse_out, 4))
     return fail(DSATTN_EINVAL, "lse_out must be 4-byte aligned");
+  if (a.rule == DSATTN_RULE_MASK) {
+    if (a.mask_in == nullptr) return fail(DSATTN_EINVAL, "mask reuse needs mask_in");
+    if (!is_device_pointer(a.mask_in)) return fail(DSATTN_EINVAL, "mask_in is not a device pointer");
+    if (a.mask_out == a.mask_in) return fail(DSATTN_EINVAL, "mask_out must not alias mask_in");
+  }
   return DSATTN_OK;
 }
 
@@ -133,6 +146,7 @@ int launch_attention(const dsattn_args& a, const Request& rq) {
   p.lse = a.lse_out;
   p.key_order = a.key_order == DSATTN_ORDER_DIAGONAL ? dsattn::kOrderDiagonal
                                                      : dsattn::kOrderAscending;
+  p.mask_in = a.rule == DSATTN_RULE_MASK ? a.mask_in : nullptr;
 
   if (p.stats != nullptr &&
       dsattn::launch_zero_u64(p.stats, (int)(bh * 4), a.stream) != hipSuccess)
@@ -231,6 +245,10 @@ int resolve_request(const dsattn_args& a, Request* rq) {
       rq->thr_log2 = (float)(lam * kLog2e);
       return DSATTN_OK;
     }
+    case DSATTN_RULE_MASK:
+      rq->rule = dsattn::kRuleMask;
+      rq->thr_log2 = 0.f;
+      return DSATTN_OK;
     case DSATTN_RULE_DYNSPARSE_LAMBDA: {
       const float lam = a.param;
       if (std::isnan(lam) || lam == INFINITY)
@@ -266,6 +284,7 @@ dsattn_args make_args(int rule, float param, const void* q, const void* k, const
   a.mask_out = nullptr;
   a.lse_out = nullptr;
   a.key_order = DSATTN_ORDER_ASCENDING;
+  a.mask_in = nullptr;
   return a;
 }
 

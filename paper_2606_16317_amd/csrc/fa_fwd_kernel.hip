@@ -70,6 +70,16 @@ struct Smem {
   alignas(4) uint8_t vote[2][kWaves];        // one byte per wave, read back as one dword
 };
 
+// Mask-reuse workgroups also hold the list of key tiles they visit (at most
+// kMaxMaskTiles, so N <= 262144 in that mode).
+constexpr int kMaxMaskTiles = 4096;
+struct MaskSmem {
+  Smem t;
+  alignas(4) uint16_t list[kMaxMaskTiles];   // (key tile << 4) | keep bit of each wave
+  alignas(4) uint16_t count[kThreads];       // kept tiles per thread, then their prefix
+  uint32_t total;                            // number of visited tiles
+};
+
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float log2_fast(float x) { return __builtin_amdgcn_logf(x); }
 __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
@@ -240,9 +250,13 @@ __device__ __forceinline__ void softmax_elem(const f32x16 (&st)[2], int e, float
 __device__ __forceinline__ void kept_tile(RowState& rs, f32x16 (&o)[4], const f32x16 (&s_cur)[2],
                                           float m_hat, float c, f32x16 (&s_next)[2],
                                           const uint16_t* kt, const uint16_t* vt,
-                                          const bf16x8 (&qf)[8], int r, int g, int lane) {
-  rescale_if_needed(rs, o, m_hat);
-  const float neg_m = -rs.m_ref;
+                                          const bf16x8 (&qf)[8], int r, int g, int lane,
+                                          bool contribute = true) {
+  // contribute == false (uniform): the tile runs the same instructions but adds nothing --
+  // exp2(S c - inf) = 0 for every element (S is finite or -inf), and the running max and
+  // sum stay as they are.
+  if (contribute) rescale_if_needed(rs, o, m_hat);
+  const float neg_m = contribute ? -rs.m_ref : -__builtin_inff();
   float psum = 0.f;
   bf16x8 pf[4];
   bf16x8 ka[3], va[3];
@@ -336,6 +350,33 @@ template <int ORDER>
 __device__ __forceinline__ int key_tile_or_past(int s, const LoopCtx& cx) {
   if constexpr (ORDER == kOrderAscending) return s;   // already past the end when s >= n_kt
   return s < cx.n_kt ? key_tile_at<ORDER>(s, cx) : cx.n_kt;
+}
+
+// Epilogue of one lane: renormalise O over the kept keys, store it as bf16, and the
+// natural-log LSE of the row over its kept keys.  A row whose unit kept no key tile
+// (possible only with a reused mask) gets zeros and -inf.
+__device__ __forceinline__ void store_rows(const FwdParams& p, const f32x16 (&o)[4],
+                                           const RowState& rs, const LoopCtx& cx,
+                                           size_t head_off, int bh, int qrow) {
+  const float l_row = half_sum(rs.l_half);
+  const bool any = l_row > 0.f;
+  const float inv = any ? 1.0f / l_row : 0.f;
+  if (cx.valid) {
+    uint16_t* orow = p.o + head_off + (size_t)qrow * kD;
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+#pragma unroll
+      for (int grp = 0; grp < 4; ++grp) {
+        bf16x4 h;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) h[i] = (__bf16)(o[db][4 * grp + i] * inv);
+        *reinterpret_cast<u32x2*>(orow + 32 * db + 8 * grp + 4 * cx.g) =
+            __builtin_bit_cast(u32x2, h);
+      }
+    if (p.lse != nullptr && cx.g == 0)
+      p.lse[(size_t)bh * cx.N + qrow] =
+          any ? (rs.m_ref + log2_fast(l_row)) * 0.69314718055994530942f : -__builtin_inff();
+  }
 }
 
 struct SkipCount {
@@ -516,24 +557,7 @@ fa_fwd_kernel(FwdParams p) {
                                        qf, sm, cx, sk);
   }
 
-  // ---- epilogue: renormalise over kept keys, store O (bf16) and the row LSE --------
-  const float l_row = half_sum(rs.l_half);
-  const float inv = 1.0f / l_row;
-  if (cx.valid) {
-    uint16_t* orow = p.o + head_off + (size_t)qrow * kD;
-#pragma unroll
-    for (int db = 0; db < 4; ++db)
-#pragma unroll
-      for (int grp = 0; grp < 4; ++grp) {
-        bf16x4 h;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) h[i] = (__bf16)(o[db][4 * grp + i] * inv);
-        *reinterpret_cast<u32x2*>(orow + 32 * db + 8 * grp + 4 * cx.g) =
-            __builtin_bit_cast(u32x2, h);
-      }
-    if (p.lse != nullptr && cx.g == 0)
-      p.lse[(size_t)bh * N + qrow] = (rs.m_ref + log2_fast(l_row)) * 0.69314718055994530942f;
-  }
+  store_rows(p, o, rs, cx, head_off, bh, qrow);
   // One set of counters per decision unit (the workgroup's tile, or each wave's rows).
   if (p.stats != nullptr && (UNIT == kTQ ? cx.w == 0 : true) && cx.lane == 0 &&
       cx.rows_valid > 0) {
@@ -543,6 +567,209 @@ fa_fwd_kernel(FwdParams p) {
     atomicAdd(st + 2, (unsigned long long)cx.rows_valid * (unsigned long long)N);
     atomicAdd(st + 3, (unsigned long long)sk.elems);
   }
+}
+
+// ---- mask reuse -----------------------------------------------------------------------
+// A skip mask from an earlier call (for instance an earlier denoising step of the same
+// layer) is applied as given: the workgroup visits only the key tiles some of its units
+// keep, in ascending order; a unit that skips a visited tile (UNIT = 32) adds nothing for
+// it.  Tiles nobody keeps cost nothing at all, not even QK^T.
+
+// Visited tiles of one workgroup, ascending: (key tile << 4) | keep bit of each wave.
+__device__ __forceinline__ int list_tile(const MaskSmem& sm, int s) {
+  return (int)__builtin_amdgcn_readfirstlane((uint32_t)sm.list[s] >> 4);
+}
+
+// One visited tile per step, with the pipeline of the dense kernel: S of the next visited
+// tile is computed while this one's softmax runs, V is requested one tile and K two tiles
+// ahead.  The list entries of steps j, j+1 and j+2 travel in registers (e0, e1, e2; past
+// the end they name the tile after the last one); the entry of step j+3 is read from LDS
+// here and used a step later, so no list read waits in front of the tile loads.
+template <int UNIT>
+__device__ __forceinline__ void mask_tile_step(int j, int n_keep, const f32x16 (&s_cur)[2],
+                                               f32x16 (&s_next)[2], float& mhat, RowState& rs,
+                                               f32x16 (&o)[4], const bf16x8 (&qf)[8],
+                                               MaskSmem& sm, const LoopCtx& cx, uint32_t& e0,
+                                               uint32_t& e1, uint32_t& e2) {
+  const int nb = (j + 1) & 1;
+  const bool has_next = j + 1 < n_keep;
+  const int tn = (int)(e1 >> 4);
+  const int tn2 = (int)(e2 >> 4);
+  const uint32_t e3_raw = j + 3 < n_keep ? (uint32_t)sm.list[j + 3]
+                                         : (uint32_t)cx.n_kt << 4;
+  bool keep_own = true;
+  if constexpr (UNIT != kTQ) keep_own = ((e0 >> cx.w) & 1u) != 0;
+  load_tile_lds(sm.t.v[nb], cx.vrs, cx.voff, tn * kTK, cx.w);
+  load_tile_lds(sm.t.k[j & 1], cx.krs, cx.koff, tn2 * kTK, cx.w);
+  // Some unit of the workgroup keeps every visited tile and the step's barrier waits for
+  // it, so a wave whose own unit skips the tile runs the kept path without contributing
+  // rather than a second code path.
+  kept_tile(rs, o, s_cur, mhat, cx.c, s_next, sm.t.k[nb], sm.t.v[j & 1], qf, cx.r, cx.g,
+            cx.lane, keep_own);
+  float mhat_next = 0.f;
+  if (has_next) {
+    if (cx.ragged && tn == cx.n_kt - 1) mask_tail(s_next, tn * kTK, cx.N, cx.g);
+    mhat_next = row_max(s_next) * cx.c;
+  }
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  mhat = mhat_next;
+  e0 = e1;
+  e1 = e2;
+  e2 = __builtin_amdgcn_readfirstlane(e3_raw);
+}
+
+template <int UNIT>
+__global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads),
+                          amdgpu_waves_per_eu(2, 2))) void
+fa_fwd_mask_kernel(FwdParams p) {
+  static_assert(UNIT == kTQ || UNIT == 32, "decision unit is the tile or one wave");
+  __shared__ __attribute__((aligned(16))) MaskSmem sm;
+
+  const int tid = threadIdx.x;
+  const int qt = blockIdx.x;
+  const int bh = blockIdx.y;
+  const int N = p.N;
+  const size_t head_off = (size_t)bh * (size_t)N * kD;
+
+  LoopCtx cx;
+  const int head_bytes = N * (kD * 2);
+  cx.krs = __builtin_amdgcn_make_buffer_rsrc((void*)(p.k + head_off), (short)0, head_bytes,
+                                             0x00020000);
+  cx.vrs = __builtin_amdgcn_make_buffer_rsrc((void*)(p.v + head_off), (short)0, head_bytes,
+                                             0x00020000);
+  cx.c = p.c;
+  cx.thr = p.thr;
+  cx.N = N;
+  cx.n_kt = p.n_kt;
+  cx.w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  cx.lane = tid & 63;
+  cx.koff = tile_lane_offset<false>(cx.w, cx.lane);
+  cx.voff = tile_lane_offset<true>(cx.w, cx.lane);
+  cx.r = cx.lane & 31;
+  cx.g = cx.lane >> 5;
+  const int q0 = qt * kTQ;
+  const int qrow = q0 + cx.w * 32 + cx.r;
+  cx.valid = qrow < N;
+  cx.ragged = (N % kTK) != 0;
+  const int unit = UNIT == kTQ ? qt : qt * (kTQ / UNIT) + cx.w;
+  cx.rows_valid = max(0, min(UNIT, N - unit * UNIT));
+
+  // ---- compact the visited tiles into sm.list ----------------------------------------
+  const int n_units = UNIT == kTQ ? 1 : kTQ / UNIT;
+  const uint8_t* rows[kTQ / 32];
+#pragma unroll
+  for (int u = 0; u < kTQ / 32; ++u) {
+    const int uu = UNIT == kTQ ? qt : qt * (kTQ / UNIT) + u;
+    rows[u] = (u < n_units && uu * UNIT < N) ? p.mask_in + ((size_t)bh * p.n_qu + uu) * p.n_kt
+                                             : nullptr;
+  }
+  auto keep_bits = [&](int t) -> uint32_t {
+    if constexpr (UNIT == kTQ) {
+      return rows[0][t] == 0 ? 0xFu : 0u;
+    } else {
+      uint32_t b = 0;
+#pragma unroll
+      for (int u = 0; u < kTQ / 32; ++u)
+        if (rows[u] != nullptr && rows[u][t] == 0) b |= 1u << u;
+      return b;
+    }
+  };
+  const int per = (cx.n_kt + kThreads - 1) / kThreads;
+  const int t_lo = min(cx.n_kt, tid * per), t_hi = min(cx.n_kt, t_lo + per);
+  uint32_t mine = 0;
+  for (int t = t_lo; t < t_hi; ++t) mine += keep_bits(t) != 0 ? 1u : 0u;
+  sm.count[tid] = (uint16_t)mine;
+  __syncthreads();
+  if (tid == 0) {
+    uint32_t run = 0;
+    for (int i = 0; i < kThreads; ++i) {
+      const uint32_t c = sm.count[i];
+      sm.count[i] = (uint16_t)run;
+      run += c;
+    }
+    sm.total = run;
+  }
+  __syncthreads();
+  {
+    uint32_t at = sm.count[tid];
+    for (int t = t_lo; t < t_hi; ++t) {
+      const uint32_t b = keep_bits(t);
+      if (b != 0) sm.list[at++] = (uint16_t)((t << 4) | b);
+    }
+  }
+  const int n_keep = (int)__builtin_amdgcn_readfirstlane(sm.total);
+
+  // The caller's mask is also the output mask; counters from this unit's own mask row.
+  if (p.mask != nullptr) {
+    for (int u = 0; u < n_units; ++u) {
+      if (rows[u] == nullptr) continue;
+      const int uu = UNIT == kTQ ? qt : qt * (kTQ / UNIT) + u;
+      uint8_t* out = p.mask + ((size_t)bh * p.n_qu + uu) * p.n_kt;
+      for (int t = tid; t < cx.n_kt; t += kThreads) out[t] = rows[u][t] != 0 ? 1 : 0;
+    }
+  }
+  if (p.stats != nullptr && (UNIT == kTQ ? cx.w == 0 : true) && cx.rows_valid > 0) {
+    const uint8_t* own = rows[UNIT == kTQ ? 0 : cx.w];
+    uint32_t skipped = 0, width = 0;
+    for (int t = cx.lane; t < cx.n_kt; t += 64)
+      if (own[t] != 0) {
+        skipped += 1;
+        width += (uint32_t)min(kTK, N - t * kTK);
+      }
+#pragma unroll
+    for (int sh = 32; sh >= 1; sh >>= 1) {
+      skipped += __shfl_xor(skipped, sh);
+      width += __shfl_xor(width, sh);
+    }
+    if (cx.lane == 0) {
+      unsigned long long* st = reinterpret_cast<unsigned long long*>(p.stats) + (size_t)bh * 4;
+      atomicAdd(st + 0, (unsigned long long)cx.n_kt);
+      atomicAdd(st + 1, (unsigned long long)skipped);
+      atomicAdd(st + 2, (unsigned long long)cx.rows_valid * (unsigned long long)N);
+      atomicAdd(st + 3, (unsigned long long)cx.rows_valid * (unsigned long long)width);
+    }
+  }
+  __syncthreads();   // the list is complete
+
+  f32x16 o[4];
+#pragma unroll
+  for (int db = 0; db < 4; ++db) o[db] = f32x16{};
+  RowState rs{-__builtin_inff(), -__builtin_inff(), 0.f};
+
+  if (n_keep > 0) {
+    const int t0 = list_tile(sm, 0);
+    load_tile_lds(sm.t.k[0], cx.krs, cx.koff, t0 * kTK, cx.w);
+    load_tile_lds(sm.t.v[0], cx.vrs, cx.voff, t0 * kTK, cx.w);
+    const uint16_t* qb = p.q + head_off;
+    bf16x8 qf[8];
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      u32x4 x = cx.valid
+                    ? *reinterpret_cast<const u32x4*>(qb + (size_t)qrow * kD + 16 * s + 8 * cx.g)
+                    : u32x4{0, 0, 0, 0};
+      qf[s] = __builtin_bit_cast(bf16x8, x);
+    }
+    load_tile_lds(sm.t.k[1], cx.krs, cx.koff, (n_keep > 1 ? list_tile(sm, 1) : cx.n_kt) * kTK,
+                  cx.w);
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+
+    f32x16 sa[2], sb[2];
+    skipped_tile(sa, sm.t.k[0], qf, cx.r, cx.g);
+    if (cx.ragged && t0 == cx.n_kt - 1) mask_tail(sa, t0 * kTK, N, cx.g);
+    float mhat = row_max(sa) * cx.c;
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+
+    const uint32_t past = (uint32_t)cx.n_kt << 4;
+    uint32_t e0 = __builtin_amdgcn_readfirstlane((uint32_t)sm.list[0]);
+    uint32_t e1 = n_keep > 1 ? __builtin_amdgcn_readfirstlane((uint32_t)sm.list[1]) : past;
+    uint32_t e2 = n_keep > 2 ? __builtin_amdgcn_readfirstlane((uint32_t)sm.list[2]) : past;
+    for (int j = 0; j < n_keep; j += 2) {
+      mask_tile_step<UNIT>(j, n_keep, sa, sb, mhat, rs, o, qf, sm, cx, e0, e1, e2);
+      if (j + 1 < n_keep)
+        mask_tile_step<UNIT>(j + 1, n_keep, sb, sa, mhat, rs, o, qf, sm, cx, e0, e1, e2);
+    }
+  }
+  store_rows(p, o, rs, cx, head_off, bh, qrow);
 }
 
 __global__ void zero_u64_kernel(uint64_t* __restrict__ p, int n) {
@@ -592,6 +819,16 @@ hipError_t launch_order(int rule, const FwdParams& p, dim3 grid, hipStream_t str
 hipError_t launch_fa_fwd(int rule, int unit_rows, const FwdParams& p, int bh,
                          hipStream_t stream) {
   const dim3 grid((unsigned)p.n_qt, (unsigned)bh);
+  if (rule == kRuleMask) {
+    if (p.n_kt > kMaxMaskTiles || p.mask_in == nullptr) return hipErrorInvalidValue;
+    if (unit_rows == kTQ)
+      hipLaunchKernelGGL((fa_fwd_mask_kernel<kTQ>), grid, dim3(kThreads), 0, stream, p);
+    else if (unit_rows == 32)
+      hipLaunchKernelGGL((fa_fwd_mask_kernel<32>), grid, dim3(kThreads), 0, stream, p);
+    else
+      return hipErrorInvalidValue;
+    return hipGetLastError();
+  }
   if (unit_rows == kTQ) return launch_order<kTQ>(rule, p, grid, stream);
   if (unit_rows == 32) return launch_order<32>(rule, p, grid, stream);
   return hipErrorInvalidValue;

@@ -7,7 +7,7 @@
 
 namespace dsattn {
 
-enum { kRuleDense = 0, kRuleBlasst = 1, kRuleDynSparse = 2 };
+enum { kRuleDense = 0, kRuleBlasst = 1, kRuleDynSparse = 2, kRuleMask = 3 };
 enum { kOrderAscending = 0, kOrderDiagonal = 1 };
 
 struct FwdParams {
@@ -25,6 +25,7 @@ struct FwdParams {
   uint8_t* mask;       // [BH][n_qu][n_kt] or null
   float* lse;          // [BH][N] or null
   int key_order;       // kOrderAscending or kOrderDiagonal
+  const uint8_t* mask_in;  // kRuleMask: [BH][n_qu][n_kt], 1 = skip (else unused)
 };
 
 // Enqueue one forward pass over `bh` heads on `stream`; unit_rows (128 or 32) is the

@@ -158,6 +158,22 @@ def test_ex_rejects_unknown_key_order():
     assert "non-null" in pkg.last_error()     # a valid order passes to the pointer checks
 
 
+def test_mask_reuse_argument_checks():
+    pkg = _lib()
+    L = pkg.lib()
+    a = pkg.DsAttnArgs(pkg.RULE_MASK, 0.0, None, None, None, None, 1, 1, 300, 128, 0.1, 128,
+                       64, None, None, None, None, pkg.ORDER_DIAGONAL, None)
+    assert L.dsattn_attn_fwd_ex(ctypes.byref(a)) == -2
+    assert "ascending" in pkg.last_error()
+    a.key_order = pkg.ORDER_ASCENDING
+    a.N = 262144 + 64
+    assert L.dsattn_attn_fwd_ex(ctypes.byref(a)) == -2
+    assert "262144" in pkg.last_error()
+    a.N = 262144                     # at the limit: passes on to the pointer checks
+    assert L.dsattn_attn_fwd_ex(ctypes.byref(a)) == -1
+    assert "non-null" in pkg.last_error()
+
+
 def test_empty_problem_is_a_no_op():
     rc, err = _fwd("dynsparse_attn_fwd", 0.95, N=0)
     assert rc == 0 and err == ""
