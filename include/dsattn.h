@@ -220,6 +220,20 @@ int dsattn_attn_fwd_reordered(const dsattn_args* args, const int32_t* q_index,
                               const int32_t* kv_index, void* workspace,
                               size_t workspace_bytes);
 
+/*
+ * MX-FP8 quantisation of bf16 rows, the storage of the quantised Q K^T variant (Section 1
+ * lists quantised attention among the methods the rule combines with).  src holds `rows`
+ * rows of `row_len` bf16 values (row_len a multiple of 32); every 32 consecutive values
+ * of a row form a block that shares the scale 2^E, E = floor(log2(max |x|)) - 8, written
+ * to `scales` as the E8M0 code E + 127 (uint8 [rows][row_len / 32]; 0 for an all-zero
+ * block), and each value becomes the FP8 E4M3 code nearest to x / 2^E in `codes` (uint8
+ * [rows][row_len]): ties to the even code, magnitudes above 448 saturate to 448, values
+ * that round to zero give +0.  Inputs must be finite.  src and codes must be 16-byte
+ * aligned device pointers; scales a device pointer.  Asynchronous on `stream`.
+ */
+int dsattn_quantize_mxfp8(const void* src, void* codes, void* scales, long long rows,
+                          int row_len, hipStream_t stream);
+
 /* Message describing the last error on this thread ("" after a successful call). */
 const char* dsattn_last_error(void);
 

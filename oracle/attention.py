@@ -200,10 +200,16 @@ def diagonal_first_order(n_kt: int, start: int) -> list:
     return sorted(range(n_kt), key=rank)
 
 
+def _as_f64(x: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns (uint16) upcast exactly, or values already given as floats."""
+    return bf16_to_f64(x) if x.dtype == np.uint16 else np.asarray(x, dtype=np.float64)
+
+
 def rule_attention(q_bits, k_bits, v_bits, scale, rule, threshold, tile_q, tile_k,
                    tiles=None, forced_mask=None, key_order="ascending",
                    order_rows=128) -> RuleRun:
-    """Run the oracle on bf16 inputs ``[B][H][N][d]`` (uint16 bit patterns).
+    """Run the oracle on bf16 inputs ``[B][H][N][d]`` (uint16 bit patterns; q and k may
+    instead be float arrays, e.g. dequantised MX-FP8 values).
 
     ``tiles``: iterable of (b, h, qi) to evaluate (default: every query tile of every
     head).  ``forced_mask``: optional uint8/bool array [B][H][T_r][T_c] of decisions to
@@ -223,11 +229,11 @@ def rule_attention(q_bits, k_bits, v_bits, scale, rule, threshold, tile_q, tile_
     cache_bh, k64, v64 = None, None, None
     for (b, h, qi) in tiles:
         if cache_bh != (b, h):
-            k64 = bf16_to_f64(k_bits[b, h])
-            v64 = bf16_to_f64(v_bits[b, h])
+            k64 = _as_f64(k_bits[b, h])
+            v64 = _as_f64(v_bits[b, h])
             cache_bh = (b, h)
         r0, r1 = qi * tile_q, min(N, (qi + 1) * tile_q)
-        q64 = bf16_to_f64(q_bits[b, h, r0:r1])
+        q64 = _as_f64(q_bits[b, h, r0:r1])
         s = scale * (q64 @ k64.T)
         forced = None if forced_mask is None else np.asarray(forced_mask[b, h, qi]).astype(bool)
         order = None

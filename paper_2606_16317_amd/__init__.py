@@ -101,6 +101,10 @@ def lib():
                                                 ctypes.c_void_p, ctypes.c_void_p,
                                                 ctypes.c_size_t]
         L.dsattn_attn_fwd_reordered.restype = ctypes.c_int
+        L.dsattn_quantize_mxfp8.argtypes = [ctypes.c_void_p] * 3 + [ctypes.c_longlong,
+                                                                      ctypes.c_int,
+                                                                      ctypes.c_void_p]
+        L.dsattn_quantize_mxfp8.restype = ctypes.c_int
         L.dsattn_last_error.argtypes = []
         L.dsattn_last_error.restype = ctypes.c_char_p
         L.dsattn_version.argtypes = []
@@ -306,6 +310,24 @@ def dsattn_scatter_rows(src, index, dst=None, stream=None):
     return dst
 
 
+def dsattn_quantize_mxfp8(x, codes=None, scales=None, stream=None):
+    """MX-FP8 codes (uint8, like x) and E8M0 block scales (uint8 [..., n / 32]) of a
+    contiguous bf16 GPU tensor whose last axis is a multiple of 32."""
+    import torch
+
+    if x.dtype != torch.bfloat16 or not x.is_cuda or not x.is_contiguous():
+        raise ValueError("x must be a contiguous bf16 GPU tensor")
+    n = int(x.shape[-1])
+    rows = x.numel() // max(1, n)
+    codes = torch.empty(x.shape, dtype=torch.uint8, device=x.device) if codes is None else codes
+    if scales is None:
+        scales = torch.empty((*x.shape[:-1], n // 32), dtype=torch.uint8, device=x.device)
+    rc = lib().dsattn_quantize_mxfp8(x.data_ptr(), codes.data_ptr(), scales.data_ptr(), rows, n,
+                                     _stream(stream))
+    _check(rc, "dsattn_quantize_mxfp8")
+    return codes, scales
+
+
 def dsattn_reordered_workspace_bytes(B, H, N, d=HEAD_DIM, with_lse=False):
     return int(lib().dsattn_reordered_workspace_bytes(B, H, N, d, int(bool(with_lse))))
 
@@ -344,5 +366,5 @@ __all__ = [
     "RULE_DYNSPARSE_LAMBDA", "RULE_MASK", "DsAttnArgs", "lib", "last_error", "dsattn_lambda_from_recall",
     "dynsparse_attn_fwd", "dynsparse_attn_fwd_lambda", "blasst_attn_fwd", "dense_attn_fwd",
     "dsattn_attn_fwd_ex", "dsattn_block_order", "dsattn_gather_rows", "dsattn_scatter_rows",
-    "dsattn_reordered_workspace_bytes", "dsattn_attn_fwd_reordered",
+    "dsattn_reordered_workspace_bytes", "dsattn_attn_fwd_reordered", "dsattn_quantize_mxfp8",
 ]

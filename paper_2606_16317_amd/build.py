@@ -20,7 +20,7 @@ LIB_NAME = "libdsattn.so"
 LIB_PATH = os.path.join(PKG_DIR, LIB_NAME)
 ARCH = "gfx950"
 
-SOURCES = ["fa_fwd_kernel.hip", "reorder_kernel.hip", "dsattn_api.cpp"]
+SOURCES = ["fa_fwd_kernel.hip", "reorder_kernel.hip", "quant_kernel.hip", "dsattn_api.cpp"]
 
 
 def hipcc() -> str:

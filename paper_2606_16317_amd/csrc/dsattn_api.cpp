@@ -12,6 +12,7 @@
 #include <string>
 
 #include "fa_fwd_launch.h"
+#include "quant_launch.h"
 #include "reorder_launch.h"
 
 namespace {
@@ -453,6 +454,33 @@ int dsattn_attn_fwd_reordered(const dsattn_args* args, const int32_t* q_index,
   if (e == hipSuccess && with_lse)
     e = dsattn::launch_scatter_rows(r.lse_out, a.lse_out, q_index, bh, a.N, 4, false, a.stream);
   if (e != hipSuccess) return fail(DSATTN_ELAUNCH, "scatter launch failed: %s", hipGetErrorString(e));
+  g_last_error.clear();
+  return DSATTN_OK;
+}
+
+int dsattn_quantize_mxfp8(const void* src, void* codes, void* scales, long long rows,
+                          int row_len, hipStream_t stream) {
+  if (rows < 0) return fail(DSATTN_EINVAL, "rows must be >= 0");
+  if (row_len <= 0 || row_len % 32 != 0)
+    return fail(DSATTN_EINVAL, "row_len must be a positive multiple of 32 (got %d)", row_len);
+  const long long n_blocks = rows * (row_len / 32);
+  if (rows > 0 && n_blocks / rows != row_len / 32) return fail(DSATTN_EINVAL, "problem too large");
+  if (n_blocks > (1LL << 40)) return fail(DSATTN_EINVAL, "problem too large");
+  if (n_blocks == 0) {
+    g_last_error.clear();
+    return DSATTN_OK;
+  }
+  const void* ptrs[] = {src, codes, scales};
+  const char* names[] = {"src", "codes", "scales"};
+  for (int i = 0; i < 3; ++i) {
+    if (ptrs[i] == nullptr) return fail(DSATTN_EINVAL, "%s must be non-null", names[i]);
+    if (!is_device_pointer(ptrs[i]))
+      return fail(DSATTN_EINVAL, "%s is not a device pointer", names[i]);
+  }
+  if (!aligned(src, 16) || !aligned(codes, 16))
+    return fail(DSATTN_EINVAL, "src and codes must be 16-byte aligned");
+  const hipError_t e = dsattn::launch_quantize_mxfp8(src, codes, scales, n_blocks, stream);
+  if (e != hipSuccess) return fail(DSATTN_ELAUNCH, "quantize launch failed: %s", hipGetErrorString(e));
   g_last_error.clear();
   return DSATTN_OK;
 }

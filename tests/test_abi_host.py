@@ -264,3 +264,21 @@ def test_reordered_rejects_bad_arguments():
     assert L.dsattn_attn_fwd_reordered(ctypes.byref(a), None, None, None, 0) == -2
     a.tile_q, a.N = 128, 0
     assert L.dsattn_attn_fwd_reordered(ctypes.byref(a), None, None, None, 0) == 0
+
+
+@pytest.mark.parametrize("rows,row_len,msg", [
+    (4, 48, "multiple of 32"), (4, 0, "multiple of 32"), (-1, 128, ">= 0"),
+    (1 << 40, 128, "too large"), (4, 128, "non-null"),
+])
+def test_quantize_rejects_bad_arguments(rows, row_len, msg):
+    rc, err = _call_raw("dsattn_quantize_mxfp8", None, None, None, rows, row_len, None)
+    assert rc == -1 and msg in err
+
+
+def test_quantize_rejects_host_pointers_and_accepts_empty():
+    buf = (ctypes.c_uint32 * 64)()
+    p = ctypes.addressof(buf)
+    rc, err = _call_raw("dsattn_quantize_mxfp8", p, p, p, 1, 32, None)
+    assert rc == -1 and "device pointer" in err
+    rc, err = _call_raw("dsattn_quantize_mxfp8", None, None, None, 0, 128, None)
+    assert rc == 0 and err == ""

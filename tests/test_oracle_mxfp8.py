@@ -109,3 +109,17 @@ def test_quantisation_error_bound():
     sat = scaled > 448.0
     assert sat.any() and rel[sat].max() < 1 - 448 / 512
     assert (scaled.reshape(50, 4, 32).max(axis=-1) >= 256).all()
+
+
+def test_rule_attention_accepts_dequantised_inputs():
+    """Float q/k inputs are used as given: bf16 values passed as floats give the same run."""
+    import oracle
+    from synth import make_random_qkv
+
+    q, k, v = make_random_qkv(1, 1, 200, 128, 3, q_std=2.0, k_std=2.0)
+    a = oracle.rule_attention(q, k, v, 0.1, "dynsparse", -4.0, 128, 64)
+    b = oracle.rule_attention(oracle.bf16_to_f64(q), oracle.bf16_to_f64(k), v, 0.1,
+                              "dynsparse", -4.0, 128, 64)
+    for ra, rb in zip(a.results, b.results):
+        assert np.array_equal(ra.skip, rb.skip)
+        np.testing.assert_array_equal(ra.o_sparse, rb.o_sparse)
