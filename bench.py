@@ -15,7 +15,9 @@ same layer as a reference point.  One JSON line is printed.
 the spatio-temporally blocked token order (``dsattn_attn_fwd_reordered``, gathers and the
 output scatter included in its time), plus the HBM rate of the row gather kernel;
 ``--reuse-sweep`` times a DynSparse call that writes its skip mask, then the mask-reuse call
-(DSATTN_RULE_MASK) that applies that mask, per threshold and decision unit.
+(DSATTN_RULE_MASK) that applies that mask, per threshold and decision unit;
+``--q8-sweep`` times the MX-FP8 quantisation of Q and K, then per rule/threshold the bf16
+call next to the call with MX-FP8 Q and K (DSATTN_QK_MXFP8).
 """
 
 from __future__ import annotations
@@ -33,6 +35,7 @@ if ROOT not in sys.path:
 
 METRIC = "effective TFLOP/s (dense-equiv) + speedup vs own dense FA at matched recall"
 PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 MFMA
+PEAK_FP8_TFLOPS = 5000.0     # MI355X dense fp8 MFMA
 HBM_PEAK_GBS = 8000.0
 TILE_Q, TILE_K, D = 128, 64, 128
 
@@ -52,6 +55,8 @@ def parse():
                     help="row-major vs blocked token order, one line per rule/threshold")
     ap.add_argument("--reuse-sweep", action="store_true",
                     help="rule call writing its mask, then mask reuse, one line per threshold")
+    ap.add_argument("--q8-sweep", action="store_true",
+                    help="bf16 vs MX-FP8 Q K^T, one line per rule/threshold")
     ap.add_argument("--q-block", default="2,8,8", help="query block (t,y,x) for --reorder-sweep")
     ap.add_argument("--kv-block", default="1,8,8", help="key/value block for --reorder-sweep")
     ap.add_argument("--calib-copy", action="store_true",
@@ -259,6 +264,8 @@ def main():
         return reorder_sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop)
     if args.reuse_sweep:
         return reuse_sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop)
+    if args.q8_sweep:
+        return q8_sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop)
 
     def step():
         dsa.dynsparse_attn_fwd(qd, kd, vd, o, scale=scale, recall_target=recall, stats_out=stats)
@@ -457,6 +464,56 @@ def reuse_sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop):
                               (reuse_ms * 1e-3) / 1e12,
                               "reuse_speedup_vs_dense": dense_ms / reuse_ms,
                               "rel_l2_vs_dense": rel}), flush=True)
+
+
+def q8_sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop):
+    import torch
+
+    B, H, N = w.B, w.H, w.N
+    qc = torch.empty(qd.shape, dtype=torch.uint8, device="cuda")
+    qs = torch.empty((B, H, N, D // 32), dtype=torch.uint8, device="cuda")
+    kc, ks = torch.empty_like(qc), torch.empty_like(qs)
+    ms = time_calls(lambda: dsa.dsattn_quantize_mxfp8(qd, qc, qs), args.steps, args.warmup)
+    moved = B * H * N * (2 * D + D + D // 32)           # bf16 in, codes and exponents out
+    print(json.dumps({"workload": w.name, "kernel": "quantize_mxfp8", "ms": ms,
+                      "roofline": {"bound": "hbm", "achieved": moved / (ms * 1e-3) / 1e9,
+                                   "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                   "frac": moved / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}}),
+          flush=True)
+    dsa.dsattn_quantize_mxfp8(kd, kc, ks)
+    rules = {"dense": dsa.RULE_DENSE, "dynsparse_recall": dsa.RULE_DYNSPARSE_RECALL,
+             "dynsparse_lambda": dsa.RULE_DYNSPARSE_LAMBDA, "blasst": dsa.RULE_BLASST}
+    points = [("dense", 0.0), ("dynsparse_recall", 0.95), ("dynsparse_lambda", -10.0),
+              ("dynsparse_lambda", -8.0), ("dynsparse_lambda", -6.0), ("blasst", 1e-2)]
+    dense_ms = None
+    for rule, p in points:
+        rec = {"workload": w.name, "rule": rule, "param": p}
+        for fmt in ("bf16", "mxfp8"):
+            out = od if (rule == "dense" and fmt == "bf16") else o
+            if fmt == "bf16":
+                fn = lambda: dsa.dsattn_attn_fwd_ex(rules[rule], p, qd, kd, vd, out, scale=scale,
+                                                    stats_out=stats)
+            else:
+                fn = lambda: dsa.dsattn_attn_fwd_mxfp8(rules[rule], p, qc, qs, kc, ks, vd, out,
+                                                       scale=scale, stats_out=stats)
+            print(f"[q8-sweep] {rule} {p} {fmt}", file=sys.stderr, flush=True)
+            ms = time_calls(fn, args.steps, args.warmup)
+            st = stats.cpu().numpy().reshape(B * H, 4)
+            if dense_ms is None:
+                dense_ms = ms
+            rel = float((out.float() - od.float()).pow(2).sum().sqrt() /
+                        od.float().pow(2).sum().sqrt())
+            elems, skipped = int(st[:, 2].sum()), int(st[:, 3].sum())
+            qk, pv = 2 * D * elems, 2 * D * (elems - skipped)
+            # time the issued MFMA work needs at peak: Q K^T at the fp8 (or bf16) rate, P V
+            # at the bf16 rate
+            t_min = qk / ((PEAK_FP8_TFLOPS if fmt == "mxfp8" else PEAK_BF16_TFLOPS) * 1e12) + \
+                pv / (PEAK_BF16_TFLOPS * 1e12)
+            rec[fmt] = {"ms": ms, "effective_tflops": dense_flop / (ms * 1e-3) / 1e12,
+                        "sparsity_tiles": float(st[:, 1].sum() / st[:, 0].sum()),
+                        "speedup_vs_bf16_dense": dense_ms / ms, "rel_l2_vs_bf16_dense": rel,
+                        "mfma_roofline_frac": t_min / (ms * 1e-3)}
+        print(json.dumps(rec), flush=True)
 
 
 if __name__ == "__main__":

@@ -69,6 +69,11 @@ typedef enum dsattn_key_order {
   DSATTN_ORDER_DIAGONAL = 1    /* from the query tile's own position outward, see below */
 } dsattn_key_order;
 
+typedef enum dsattn_qk_format {
+  DSATTN_QK_BF16 = 0,   /* q and k are bf16 [B][H][N][d] */
+  DSATTN_QK_MXFP8 = 1   /* q and k are MX-FP8 codes with E8M0 exponents, see below */
+} dsattn_qk_format;
+
 typedef enum dsattn_rule {
   DSATTN_RULE_DENSE = 0,
   DSATTN_RULE_BLASST = 1,            /* param = tau in [0, 1] */
@@ -134,6 +139,9 @@ typedef struct dsattn_args {
   float* lse_out;        /* may be NULL */
   int key_order;         /* dsattn_key_order; the named entry points use ascending */
   const uint8_t* mask_in; /* DSATTN_RULE_MASK only, else ignored (see below) */
+  int qk_format;         /* dsattn_qk_format; the named entry points use bf16 */
+  const uint8_t* q_scales; /* DSATTN_QK_MXFP8 only, else ignored (see below) */
+  const uint8_t* k_scales;
 } dsattn_args;
 
 /*
@@ -159,6 +167,17 @@ int dsattn_attn_fwd_ex(const dsattn_args* args);
  * ascending order) reproduces that call's output bit for bit.  Requirements: mask_in
  * non-NULL, key_order ascending, ceil(N/tile_k) <= 4096 (N <= 262144), else
  * DSATTN_EINVAL / DSATTN_EUNSUPPORTED.  mask_out, if given, receives mask_in (as 0/1).
+ */
+
+/*
+ * Quantised Q K^T (DSATTN_QK_MXFP8; Section 1 lists quantised attention among the methods
+ * the rule combines with).  q and k then point at E4M3 codes (uint8 [B][H][N][d], 16-byte
+ * aligned) and q_scales / k_scales at their E8M0 block exponents (uint8 [B][H][N][d/32],
+ * 4-byte aligned), as written by dsattn_quantize_mxfp8: element x of block b of a row
+ * stands for e4m3(x) * 2^(scale[b] - 127).  S = Q K^T is computed from these values with
+ * fp32 accumulation; v stays bf16, and the rule, the softmax and P V are as in the bf16
+ * path.  Supported for the dense, BLASST and DynSparse rules with tile_q = 128 and
+ * ascending key order (DSATTN_EUNSUPPORTED otherwise), not by the reordered entry point.
  */
 
 /*

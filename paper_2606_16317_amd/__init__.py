@@ -35,6 +35,9 @@ RULE_MASK = 4
 ORDER_ASCENDING = 0
 ORDER_DIAGONAL = 1
 
+QK_BF16 = 0
+QK_MXFP8 = 1
+
 _lib = None
 
 
@@ -61,6 +64,9 @@ class DsAttnArgs(ctypes.Structure):
         ("lse_out", ctypes.c_void_p),
         ("key_order", ctypes.c_int),
         ("mask_in", ctypes.c_void_p),
+        ("qk_format", ctypes.c_int),
+        ("q_scales", ctypes.c_void_p),
+        ("k_scales", ctypes.c_void_p),
     ]
 
 
@@ -258,6 +264,31 @@ def dsattn_attn_fwd_ex(rule, param, q, k, v, o=None, scale=None, tile_q=TILE_Q,
     return o
 
 
+def dsattn_attn_fwd_mxfp8(rule, param, q8, q_scales, k8, k_scales, v, o=None, scale=None,
+                          stats_out=None, mask_out=None, lse_out=None, stream=None):
+    """A rule with MX-FP8 Q and K (``dsattn_qk_format`` DSATTN_QK_MXFP8): q8 / k8 are uint8
+    E4M3 codes [B, H, N, 128] and q_scales / k_scales their uint8 E8M0 exponents
+    [B, H, N, 4], as returned by ``dsattn_quantize_mxfp8``; v is bf16.  tile_q is 128 and
+    the key order ascending."""
+    import torch
+
+    o = torch.empty_like(v) if o is None else o
+    B, H, N, d = _shape(v, v, v, o)
+    for name, t, n in (("q8", q8, d), ("k8", k8, d), ("q_scales", q_scales, d // 32),
+                       ("k_scales", k_scales, d // 32)):
+        if not isinstance(t, torch.Tensor) or t.dtype != torch.uint8:
+            raise TypeError(f"{name} must be a uint8 tensor")
+        if not t.is_cuda or not t.is_contiguous() or tuple(t.shape) != (B, H, N, n):
+            raise ValueError(f"{name} must be a contiguous GPU tensor of shape {(B, H, N, n)}")
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    st, mk, ls = _buffers(B, H, N, stats_out, mask_out, lse_out, TILE_Q)
+    a = DsAttnArgs(rule, param, q8.data_ptr(), k8.data_ptr(), v.data_ptr(), o.data_ptr(),
+                   B, H, N, d, scale, TILE_Q, TILE_K, _stream(stream), st, mk, ls,
+                   ORDER_ASCENDING, None, QK_MXFP8, q_scales.data_ptr(), k_scales.data_ptr())
+    _check(lib().dsattn_attn_fwd_ex(ctypes.byref(a)), "dsattn_attn_fwd_ex")
+    return o
+
+
 def dsattn_block_order(grid, block):
     """Gather map (numpy int32 [T*Y*X]) of the blocked token order, computed by the
     library's host code: position i of the reordered sequence holds token perm[i]."""
@@ -367,4 +398,5 @@ __all__ = [
     "dynsparse_attn_fwd", "dynsparse_attn_fwd_lambda", "blasst_attn_fwd", "dense_attn_fwd",
     "dsattn_attn_fwd_ex", "dsattn_block_order", "dsattn_gather_rows", "dsattn_scatter_rows",
     "dsattn_reordered_workspace_bytes", "dsattn_attn_fwd_reordered", "dsattn_quantize_mxfp8",
+    "dsattn_attn_fwd_mxfp8", "QK_BF16", "QK_MXFP8",
 ]

@@ -73,6 +73,16 @@ int check_problem(const dsattn_args& a) {
     return fail(DSATTN_EINVAL, "problem too large");
   if (a.key_order != DSATTN_ORDER_ASCENDING && a.key_order != DSATTN_ORDER_DIAGONAL)
     return fail(DSATTN_EINVAL, "unknown key order %d", a.key_order);
+  if (a.qk_format != DSATTN_QK_BF16 && a.qk_format != DSATTN_QK_MXFP8)
+    return fail(DSATTN_EINVAL, "unknown qk format %d", a.qk_format);
+  if (a.qk_format == DSATTN_QK_MXFP8) {
+    if (a.rule == DSATTN_RULE_MASK)
+      return fail(DSATTN_EUNSUPPORTED, "mask reuse takes bf16 q and k");
+    if (a.tile_q != kTileQ)
+      return fail(DSATTN_EUNSUPPORTED, "MX-FP8 q and k need tile_q = 128");
+    if (a.key_order != DSATTN_ORDER_ASCENDING)
+      return fail(DSATTN_EUNSUPPORTED, "MX-FP8 q and k need the ascending key order");
+  }
   if (a.rule == DSATTN_RULE_MASK) {
     if (a.key_order != DSATTN_ORDER_ASCENDING)
       return fail(DSATTN_EUNSUPPORTED, "mask reuse visits key tiles in ascending order only");
@@ -107,6 +117,14 @@ int check_pointers(const dsattn_args& a) {
     return fail(DSATTN_EINVAL, "lse_out is not a device pointer");
   if (a.lse_out != nullptr && !aligned(a.lse_out, 4))
     return fail(DSATTN_EINVAL, "lse_out must be 4-byte aligned");
+  if (a.qk_format == DSATTN_QK_MXFP8) {
+    if (a.q_scales == nullptr || a.k_scales == nullptr)
+      return fail(DSATTN_EINVAL, "MX-FP8 q and k need q_scales and k_scales");
+    if (!is_device_pointer(a.q_scales) || !is_device_pointer(a.k_scales))
+      return fail(DSATTN_EINVAL, "q_scales and k_scales must be device pointers");
+    if (!aligned(a.q_scales, 4) || !aligned(a.k_scales, 4))
+      return fail(DSATTN_EINVAL, "q_scales and k_scales must be 4-byte aligned");
+  }
   if (a.rule == DSATTN_RULE_MASK) {
     if (a.mask_in == nullptr) return fail(DSATTN_EINVAL, "mask reuse needs mask_in");
     if (!is_device_pointer(a.mask_in)) return fail(DSATTN_EINVAL, "mask_in is not a device pointer");
@@ -148,6 +166,13 @@ int launch_attention(const dsattn_args& a, const Request& rq) {
   p.key_order = a.key_order == DSATTN_ORDER_DIAGONAL ? dsattn::kOrderDiagonal
                                                      : dsattn::kOrderAscending;
   p.mask_in = a.rule == DSATTN_RULE_MASK ? a.mask_in : nullptr;
+  const bool q8 = a.qk_format == DSATTN_QK_MXFP8;
+  p.qk_format = q8 ? dsattn::kQkMxfp8 : dsattn::kQkBf16;
+  p.q8 = q8 ? static_cast<const uint8_t*>(a.q) : nullptr;
+  p.k8 = q8 ? static_cast<const uint8_t*>(a.k) : nullptr;
+  p.q_scales = q8 ? a.q_scales : nullptr;
+  p.k_scales = q8 ? a.k_scales : nullptr;
+  if (q8) p.q = p.k = nullptr;
 
   if (p.stats != nullptr &&
       dsattn::launch_zero_u64(p.stats, (int)(bh * 4), a.stream) != hipSuccess)
@@ -286,6 +311,9 @@ dsattn_args make_args(int rule, float param, const void* q, const void* k, const
   a.lse_out = nullptr;
   a.key_order = DSATTN_ORDER_ASCENDING;
   a.mask_in = nullptr;
+  a.qk_format = DSATTN_QK_BF16;
+  a.q_scales = nullptr;
+  a.k_scales = nullptr;
   return a;
 }
 
@@ -405,6 +433,8 @@ int dsattn_attn_fwd_reordered(const dsattn_args* args, const int32_t* q_index,
   int rc = resolve_request(a, &rq);
   if (rc != DSATTN_OK) return rc;
   if ((rc = check_problem(a)) != DSATTN_OK) return rc;
+  if (a.qk_format != DSATTN_QK_BF16)
+    return fail(DSATTN_EUNSUPPORTED, "the reordered entry point takes bf16 q and k");
   if (empty_problem(a)) return finish_empty(a);
   if ((rc = check_pointers(a)) != DSATTN_OK) return rc;
   if (q_index == nullptr || kv_index == nullptr || workspace == nullptr)

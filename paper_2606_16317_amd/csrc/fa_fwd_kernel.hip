@@ -54,6 +54,7 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef int i32x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kD = 128;        // head dimension
 constexpr int kTQ = 128;       // query rows per workgroup (decision granularity)
@@ -65,9 +66,10 @@ constexpr int kTileElems = kTK * kD;         // 8192 bf16 = 16 KiB
 constexpr float kRescaleSlack = 8.0f;        // log2 units
 
 struct Smem {
-  alignas(16) uint16_t k[2][kTileElems];
+  alignas(16) uint16_t k[2][kTileElems];     // bf16 K tiles, or MX-FP8 K tiles (first half)
   alignas(16) uint16_t v[2][kTileElems];
   alignas(4) uint8_t vote[2][kWaves];        // one byte per wave, read back as one dword
+  alignas(16) uint8_t ks[2][kTK * 4];        // MX-FP8 K: E8M0 exponents, 4 blocks per key
 };
 
 // Mask-reuse workgroups also hold the list of key tiles they visit (at most
@@ -166,6 +168,136 @@ __device__ __forceinline__ bf16x4 lds_tr_b64(const uint16_t* p) {
   typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
   const i16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p));
   return __builtin_bit_cast(bf16x4, x);
+}
+
+// ---- MX-FP8 Q K^T ------------------------------------------------------------------
+// Quantised Q and K (E4M3 values, one E8M0 exponent per 32 values of a row) feed
+// v_mfma_scale_f32_32x32x64_f8f6f4, which multiplies a 32 x 64 block of K by a 64 x 32
+// block of Q^T and applies the exponents itself.  In its operands lane l holds row l % 32
+// and 32 bytes.  Bytes 0-15 of both lane halves form the first 32-value exponent block of
+// the 64-wide step and bytes 16-31 the second; the exponent of the first block comes from
+// the lane of the low half, that of the second from the lane of the high half (measured
+// with an in-bounds probe).  So for d-step s, lane half g reads d in [64 s + 16 g, +16)
+// and [64 s + 32 + 16 g, +16) and supplies the exponent of block 2 s + g of its row.
+//
+// The fp8 K tile (64 keys x 128 bytes = 8 KiB) lives in 32 lines of 256 bytes: line L
+// holds key L in its first 128 bytes and key L + 32 in its last 128, in 16-byte chunks
+// XOR-swizzled by L % 16 like the bf16 tiles, so every 16-lane group of an operand read
+// touches each bank once.
+
+__device__ __forceinline__ int k8_slot(int line, int half, int chunk) {
+  return (8 * half + chunk) ^ (line & 15);
+}
+
+// Lane offset (bytes, relative to the tile's first key) of wave w's first 1 KiB block of
+// the fp8 K tile (lines 4 w .. 4 w + 3); its second block, 16 lines on, holds keys 16
+// further on: 2 KiB further in global memory.
+__device__ __forceinline__ uint32_t k8_lane_offset(int w, int lane) {
+  const int line = 4 * w + (lane >> 4);       // line of this lane's slot
+  const int s = (lane & 15) ^ (line & 15);    // logical chunk stored in that slot
+  const int key = line + 32 * (s >> 3);
+  return (uint32_t)(key * kD + (s & 7) * 16);
+}
+
+// Copy the fp8 K tile starting at key key0 into LDS (two 1 KiB blocks per wave) and, from
+// wave 0, the tile's exponents (one dword per key).  Keys >= N come back as zeros.
+__device__ __forceinline__ void load_k8_tile(uint8_t* tile, uint8_t* scales,
+                                             __amdgpu_buffer_rsrc_t rs,
+                                             __amdgpu_buffer_rsrc_t srs, uint32_t off,
+                                             int key0, int w, int lane) {
+  const uint32_t o0 = off + (uint32_t)key0 * kD;
+  const uint32_t lds0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(tile + w * 1024));
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %[sv], m0\n\t"
+      "s_mov_b32 m0, %[l0]\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %[o0], %[rs], 0 offen lds\n\t"
+      "s_add_u32 m0, %[l0], 0x1000\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %[o1], %[rs], 0 offen lds\n\t"
+      "s_mov_b32 m0, %[sv]"
+      : [sv] "=&s"(saved)
+      : [l0] "s"(lds0), [o0] "v"(o0), [o1] "v"(o0 + 2048u), [rs] "s"(rs)
+      : "memory", "scc");
+  if (w == 0) {
+    const uint32_t s0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)scales);
+    const uint32_t so = ((uint32_t)key0 + (uint32_t)lane) * 4u;
+    asm volatile(
+        "s_mov_b32 %[sv], m0\n\t"
+        "s_mov_b32 m0, %[l0]\n\t"
+        "s_nop 0\n\t"
+        "buffer_load_dword %[o0], %[rs], 0 offen lds\n\t"
+        "s_mov_b32 m0, %[sv]"
+        : [sv] "=&s"(saved)
+        : [l0] "s"(s0), [o0] "v"(so), [rs] "s"(srs)
+        : "memory", "scc");
+  }
+}
+
+// K operand of key block kb (keys 32 kb + r) and d-step s for lane half g.
+__device__ __forceinline__ i32x8 k8_operand(const uint8_t* kt, int kb, int s, int r, int g) {
+  const uint8_t* line = kt + r * 256;
+  const u32x4 lo = *reinterpret_cast<const u32x4*>(line + k8_slot(r, kb, 4 * s + g) * 16);
+  const u32x4 hi = *reinterpret_cast<const u32x4*>(line + k8_slot(r, kb, 4 * s + 2 + g) * 16);
+  return i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3],
+               (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+}
+
+// Exponent word of key 32 kb + r for lane half g: byte 0 = block g (d-step 0), byte 2 =
+// block 2 + g (d-step 1), picked by the MFMA's op_sel.
+__device__ __forceinline__ uint32_t k8_scales(const uint8_t* ks, int kb, int r, int g) {
+  const uint32_t w = *reinterpret_cast<const uint32_t*>(ks + (32 * kb + r) * 4);
+  return (w >> (8 * g)) & 0x00ff00ffu;
+}
+
+// One MX-FP8 MFMA of d-step S (exponent byte 2 S of both scale words).  The empty
+// statement after it reads the result together with a and b, so all three are live at
+// once and the result registers never share storage with the operands (with a zero
+// accumulator the compiler would otherwise reuse their registers, which gives wrong
+// results for this instruction).
+template <int S>
+__device__ __forceinline__ f32x16 mfma_q8(const i32x8& a, const i32x8& b, const f32x16& acc,
+                                          uint32_t sa, uint32_t sb) {
+  f32x16 r = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+      a, b, acc, 0, 0, (S == 0 ? 0 : 2), (int)sa, (S == 0 ? 0 : 2), (int)sb);
+  asm volatile("" : "+v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
+// Q^T operand registers of one lane in the MX-FP8 path: both d-steps and the exponent word.
+struct QFrag8 {
+  i32x8 q[2];
+  uint32_t sc;
+};
+
+// K^T operand registers of one lane for the current tile: the first d-step of both key
+// blocks (refilled with the second d-step as the MFMAs consume them) and the exponents.
+struct KFrag8 {
+  i32x8 a[2];
+  uint32_t sc[2];
+};
+
+__device__ __forceinline__ void k8_begin(KFrag8& kf, const uint8_t* kt, const uint8_t* ks,
+                                         int r, int g) {
+  kf.sc[0] = k8_scales(ks, 0, r, g);
+  kf.sc[1] = k8_scales(ks, 1, r, g);
+  kf.a[0] = k8_operand(kt, 0, 0, r, g);
+  kf.a[1] = k8_operand(kt, 1, 0, r, g);
+}
+
+// MFMA i (0..3) of S^T = K Q^T on the MX-FP8 path: key block i % 2, d-step i / 2.  The two
+// first-step MFMAs also refill their block's operand with the second d-step.
+__device__ __forceinline__ void qk_q8_step(int i, f32x16 (&s_next)[2], KFrag8& kf,
+                                           const uint8_t* kt, const QFrag8& qf, int r, int g) {
+  const int kb = i & 1;
+  const i32x8 a = kf.a[kb];
+  if (i < 2) {
+    kf.a[kb] = k8_operand(kt, kb, 1, r, g);
+    s_next[kb] = mfma_q8<0>(a, qf.q[0], f32x16{}, kf.sc[kb], qf.sc);
+  } else {
+    s_next[kb] = mfma_q8<1>(a, qf.q[1], s_next[kb], kf.sc[kb], qf.sc);
+  }
 }
 
 // K operand of S^T MFMA number i (chains alternate: block b = i % 2, d step s = i / 2).
@@ -287,6 +419,41 @@ __device__ __forceinline__ void kept_tile(RowState& rs, f32x16 (&o)[4], const f3
   __builtin_amdgcn_s_setprio(0);
 }
 
+// Kept tile j on the MX-FP8 path: as kept_tile, with S_{j+1} from four scaled fp8 MFMAs
+// that carry eight softmax elements each.  (The P V loop is written out in both tile
+// bodies: moving it into a shared inline function changes the bf16 kernel's schedule.)
+__device__ __forceinline__ void kept_tile_q8(RowState& rs, f32x16 (&o)[4],
+                                             const f32x16 (&s_cur)[2], float m_hat, float c,
+                                             f32x16 (&s_next)[2], const uint8_t* kt,
+                                             const uint8_t* ks, const uint16_t* vt,
+                                             const QFrag8& qf, int r, int g, int lane) {
+  rescale_if_needed(rs, o, m_hat);
+  const float neg_m = -rs.m_ref;
+  float psum = 0.f;
+  bf16x8 pf[4];
+  bf16x8 va[3];
+  KFrag8 kf;
+  k8_begin(kf, kt, ks, r, g);
+  sched_fence();
+  __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    qk_q8_step(i, s_next, kf, kt, qf, r, g);
+    if (i >= 2) va[i - 2] = v_operand(vt, i - 2, lane);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) softmax_elem(s_cur, 8 * i + e, c, neg_m, psum, pf);
+    sched_fence();
+  }
+  rs.l_half += psum;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    if (i + 2 < 16) va[(i + 2) % 3] = v_operand(vt, i + 2, lane);
+    o[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i % 3], pf[i >> 2], o[i & 3], 0, 0, 0);
+    sched_fence();
+  }
+  __builtin_amdgcn_s_setprio(0);
+}
+
 // Skipped tile j: only S_{j+1} = K_{j+1} Q^T.
 __device__ __forceinline__ void skipped_tile(f32x16 (&s_next)[2], const uint16_t* kt,
                                              const bf16x8 (&qf)[8], int r, int g) {
@@ -304,6 +471,30 @@ __device__ __forceinline__ void skipped_tile(f32x16 (&s_next)[2], const uint16_t
   }
 }
 
+// Skipped tile j on the MX-FP8 path: only S_{j+1}.
+__device__ __forceinline__ void skipped_tile_q8(f32x16 (&s_next)[2], const uint8_t* kt,
+                                                const uint8_t* ks, const QFrag8& qf, int r,
+                                                int g) {
+  KFrag8 kf;
+  k8_begin(kf, kt, ks, r, g);
+  sched_fence();
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    qk_q8_step(i, s_next, kf, kt, qf, r, g);
+    sched_fence();
+  }
+}
+
+// Q operand registers of the bf16 path (eight d-steps) and of the MX-FP8 path.
+template <bool Q8>
+struct QFragOf {
+  typedef bf16x8 type[8];
+};
+template <>
+struct QFragOf<true> {
+  typedef QFrag8 type;
+};
+
 template <int RULE>
 __device__ __forceinline__ bool row_keeps(const RowState& rs, float m_hat, float thr) {
   if constexpr (RULE == kRuleDynSparse) {
@@ -318,6 +509,7 @@ __device__ __forceinline__ bool row_keeps(const RowState& rs, float m_hat, float
 struct LoopCtx {
   __amdgpu_buffer_rsrc_t krs;   // K / V of this head as buffer resources
   __amdgpu_buffer_rsrc_t vrs;
+  __amdgpu_buffer_rsrc_t ksrs;  // MX-FP8 path: the exponents of K (4 bytes per key)
   uint32_t koff, voff;          // lane offsets inside a 1 KiB tile block
   uint8_t* mask_row;            // this decision unit's row of the skip mask, or null
   float c;
@@ -384,6 +576,17 @@ struct SkipCount {
   uint64_t elems = 0;
 };
 
+// Stage the K tile starting at key key0 into K buffer buf (bf16, or MX-FP8 codes and
+// exponents).
+template <bool Q8>
+__device__ __forceinline__ void load_k_tile(Smem& sm, int buf, const LoopCtx& cx, int key0) {
+  if constexpr (Q8)
+    load_k8_tile(reinterpret_cast<uint8_t*>(sm.k[buf]), sm.ks[buf], cx.krs, cx.ksrs, cx.koff,
+                 key0, cx.w, cx.lane);
+  else
+    load_tile_lds(sm.k[buf], cx.krs, cx.koff, key0, cx.w);
+}
+
 // One loop step j, visiting key tile key_tile_at(j) (written "tile j" below; LDS buffers
 // rotate with the step).  On entry s_cur holds S_j, mhat its row max (log2 units), keep_own
 // the decision for tile j of this wave's decision unit (the workgroup's 128 query rows,
@@ -396,11 +599,11 @@ struct SkipCount {
 // ahead when tile j is kept (runs of kept tiles are the common case); after a skipped
 // tile, a kept tile's V is requested at the start of its own iteration, so a run of
 // skipped tiles streams K alone.
-template <int RULE, int UNIT, int ORDER>
+template <int RULE, int UNIT, int ORDER, bool Q8>
 __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f32x16 (&s_next)[2],
                                               float& mhat, bool& keep_own, bool& keep_any,
                                               bool& v_ready, RowState& rs, f32x16 (&o)[4],
-                                              const bf16x8 (&qf)[8], Smem& sm,
+                                              const typename QFragOf<Q8>::type& qf, Smem& sm,
                                               const LoopCtx& cx, SkipCount& sk) {
   const int nb = (j + 1) & 1;
   const bool has_next = (j + 1) < cx.n_kt;
@@ -421,16 +624,25 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
     asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
   }
   if (keep_any) load_tile_lds(sm.v[nb], cx.vrs, cx.voff, tn * kTK, cx.w);
-  load_tile_lds(sm.k[j & 1], cx.krs, cx.koff, tn2 * kTK, cx.w);
+  load_k_tile<Q8>(sm, j & 1, cx, tn2 * kTK);
 
   // S_{j+1} is computed on both paths (on the last tile it reads a stale buffer and is
   // dropped).
   if (keep_own) {
-    kept_tile(rs, o, s_cur, mhat, cx.c, s_next, sm.k[nb], sm.v[j & 1], qf, cx.r, cx.g, cx.lane);
+    if constexpr (Q8)
+      kept_tile_q8(rs, o, s_cur, mhat, cx.c, s_next, reinterpret_cast<const uint8_t*>(sm.k[nb]),
+                   sm.ks[nb], sm.v[j & 1], qf, cx.r, cx.g, cx.lane);
+    else
+      kept_tile(rs, o, s_cur, mhat, cx.c, s_next, sm.k[nb], sm.v[j & 1], qf, cx.r, cx.g,
+                cx.lane);
   } else {
     sk.tiles += 1;
     sk.elems += (uint64_t)cx.rows_valid * (uint64_t)min(kTK, cx.N - tj * kTK);
-    skipped_tile(s_next, sm.k[nb], qf, cx.r, cx.g);
+    if constexpr (Q8)
+      skipped_tile_q8(s_next, reinterpret_cast<const uint8_t*>(sm.k[nb]), sm.ks[nb], qf, cx.r,
+                      cx.g);
+    else
+      skipped_tile(s_next, sm.k[nb], qf, cx.r, cx.g);
   }
   v_ready = keep_any;
 
@@ -460,7 +672,9 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
 
 // UNIT: query rows per skip decision, 128 (the workgroup's tile) or 32 (one wave).
 // ORDER: key-tile visit order (ascending or diagonal-first).
-template <int RULE, int UNIT, int ORDER>
+// Q8: Q and K in MX-FP8 (codes p.q8 / p.k8, exponents p.q_scales / p.k_scales), S = Q K^T
+// on the scaled fp8 MFMA; everything after S is the same as with bf16 Q and K.
+template <int RULE, int UNIT, int ORDER, bool Q8>
 __global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads),
                           amdgpu_waves_per_eu(2, 2))) void
 fa_fwd_kernel(FwdParams p) {
@@ -486,8 +700,15 @@ fa_fwd_kernel(FwdParams p) {
 
   LoopCtx cx;
   const int head_bytes = N * (kD * 2);
-  cx.krs = __builtin_amdgcn_make_buffer_rsrc((void*)(p.k + head_off), (short)0, head_bytes,
-                                             0x00020000);
+  if constexpr (Q8) {
+    cx.krs = __builtin_amdgcn_make_buffer_rsrc((void*)(p.k8 + head_off), (short)0, N * kD,
+                                               0x00020000);
+    cx.ksrs = __builtin_amdgcn_make_buffer_rsrc((void*)(p.k_scales + (size_t)bh * N * 4),
+                                                (short)0, N * 4, 0x00020000);
+  } else {
+    cx.krs = __builtin_amdgcn_make_buffer_rsrc((void*)(p.k + head_off), (short)0, head_bytes,
+                                               0x00020000);
+  }
   cx.vrs = __builtin_amdgcn_make_buffer_rsrc((void*)(p.v + head_off), (short)0, head_bytes,
                                              0x00020000);
   cx.c = p.c;
@@ -496,7 +717,7 @@ fa_fwd_kernel(FwdParams p) {
   cx.n_kt = p.n_kt;
   cx.w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index, kept in an SGPR
   cx.lane = tid & 63;
-  cx.koff = tile_lane_offset<false>(cx.w, cx.lane);
+  cx.koff = Q8 ? k8_lane_offset(cx.w, cx.lane) : tile_lane_offset<false>(cx.w, cx.lane);
   cx.voff = tile_lane_offset<true>(cx.w, cx.lane);
   cx.r = cx.lane & 31;
   cx.g = cx.lane >> 5;
@@ -517,29 +738,52 @@ fa_fwd_kernel(FwdParams p) {
 
   // Stage K and V of the first visited tile, then K of the second.
   const int t0 = key_tile_at<ORDER>(0, cx);
-  load_tile_lds(sm.k[0], cx.krs, cx.koff, t0 * kTK, cx.w);
+  load_k_tile<Q8>(sm, 0, cx, t0 * kTK);
   load_tile_lds(sm.v[0], cx.vrs, cx.voff, t0 * kTK, cx.w);
 
-  // Q^T B-operand fragments: d = 16 s + 8 g + (0..7) of this lane's query row.
-  const uint16_t* qb = p.q + head_off;
-  bf16x8 qf[8];
+  typename QFragOf<Q8>::type qf;
+  if constexpr (Q8) {
+    // d in [64 s + 16 g, +16) and [64 s + 32 + 16 g, +16) of the row for d-step s; the
+    // exponent word carries blocks g (byte 0) and 2 + g (byte 2).
+    const uint8_t* qrow8 = p.q8 + head_off + (size_t)qrow * kD;
 #pragma unroll
-  for (int s = 0; s < 8; ++s) {
-    u32x4 x = cx.valid
-                  ? *reinterpret_cast<const u32x4*>(qb + (size_t)qrow * kD + 16 * s + 8 * cx.g)
-                  : u32x4{0, 0, 0, 0};
-    qf[s] = __builtin_bit_cast(bf16x8, x);
+    for (int s = 0; s < 2; ++s) {
+      const u32x4 lo = cx.valid ? *reinterpret_cast<const u32x4*>(qrow8 + 64 * s + 16 * cx.g)
+                                : u32x4{0, 0, 0, 0};
+      const u32x4 hi = cx.valid
+                           ? *reinterpret_cast<const u32x4*>(qrow8 + 64 * s + 32 + 16 * cx.g)
+                           : u32x4{0, 0, 0, 0};
+      qf.q[s] = i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3],
+                      (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+    }
+    const uint32_t qs =
+        cx.valid ? *reinterpret_cast<const uint32_t*>(p.q_scales + ((size_t)bh * N + qrow) * 4)
+                 : 0u;
+    qf.sc = (qs >> (8 * cx.g)) & 0x00ff00ffu;
+  } else {
+    // Q^T B-operand fragments: d = 16 s + 8 g + (0..7) of this lane's query row.
+    const uint16_t* qb = p.q + head_off;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      u32x4 x = cx.valid
+                    ? *reinterpret_cast<const u32x4*>(qb + (size_t)qrow * kD + 16 * s + 8 * cx.g)
+                    : u32x4{0, 0, 0, 0};
+      qf[s] = __builtin_bit_cast(bf16x8, x);
+    }
   }
   f32x16 o[4];
 #pragma unroll
   for (int db = 0; db < 4; ++db) o[db] = f32x16{};
   RowState rs{-__builtin_inff(), -__builtin_inff(), 0.f};
 
-  load_tile_lds(sm.k[1], cx.krs, cx.koff, key_tile_or_past<ORDER>(1, cx) * kTK, cx.w);
+  load_k_tile<Q8>(sm, 1, cx, key_tile_or_past<ORDER>(1, cx) * kTK);
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 
   f32x16 sa[2], sb[2];
-  skipped_tile(sa, sm.k[0], qf, cx.r, cx.g);   // S of the first visited tile
+  if constexpr (Q8)                            // S of the first visited tile
+    skipped_tile_q8(sa, reinterpret_cast<const uint8_t*>(sm.k[0]), sm.ks[0], qf, cx.r, cx.g);
+  else
+    skipped_tile(sa, sm.k[0], qf, cx.r, cx.g);
   if (cx.ragged && t0 == cx.n_kt - 1) mask_tail(sa, t0 * kTK, N, cx.g);
   float mhat = row_max(sa) * cx.c;
   bool keep_own = true;                      // the first tile is always kept
@@ -550,11 +794,11 @@ fa_fwd_kernel(FwdParams p) {
 
   // Unrolled by two so that S_j / S_{j+1} alternate between sa and sb without copies.
   for (int j = 0; j < cx.n_kt; j += 2) {
-    key_tile_step<RULE, UNIT, ORDER>(j, sa, sb, mhat, keep_own, keep_any, v_ready, rs, o, qf,
-                                     sm, cx, sk);
+    key_tile_step<RULE, UNIT, ORDER, Q8>(j, sa, sb, mhat, keep_own, keep_any, v_ready, rs, o,
+                                         qf, sm, cx, sk);
     if (j + 1 < cx.n_kt)
-      key_tile_step<RULE, UNIT, ORDER>(j + 1, sb, sa, mhat, keep_own, keep_any, v_ready, rs, o,
-                                       qf, sm, cx, sk);
+      key_tile_step<RULE, UNIT, ORDER, Q8>(j + 1, sb, sa, mhat, keep_own, keep_any, v_ready, rs,
+                                           o, qf, sm, cx, sk);
   }
 
   store_rows(p, o, rs, cx, head_off, bh, qrow);
@@ -781,22 +1025,23 @@ __global__ void zero_u64_kernel(uint64_t* __restrict__ p, int n) {
 
 namespace {
 
-template <int UNIT, int ORDER>
+template <int UNIT, int ORDER, bool Q8 = false>
 hipError_t launch_unit(int rule, const FwdParams& p, dim3 grid, hipStream_t stream) {
   const dim3 block(kThreads);
   switch (rule) {
     case kRuleDense:
       // Every tile is kept, so the visit order changes nothing but the rounding of the
       // sums: the dense kernel always walks ascending.
-      hipLaunchKernelGGL((fa_fwd_kernel<kRuleDense, UNIT, kOrderAscending>), grid, block, 0,
+      hipLaunchKernelGGL((fa_fwd_kernel<kRuleDense, UNIT, kOrderAscending, Q8>), grid, block, 0,
                          stream, p);
       break;
     case kRuleBlasst:
-      hipLaunchKernelGGL((fa_fwd_kernel<kRuleBlasst, UNIT, ORDER>), grid, block, 0, stream, p);
+      hipLaunchKernelGGL((fa_fwd_kernel<kRuleBlasst, UNIT, ORDER, Q8>), grid, block, 0, stream,
+                         p);
       break;
     case kRuleDynSparse:
-      hipLaunchKernelGGL((fa_fwd_kernel<kRuleDynSparse, UNIT, ORDER>), grid, block, 0, stream,
-                         p);
+      hipLaunchKernelGGL((fa_fwd_kernel<kRuleDynSparse, UNIT, ORDER, Q8>), grid, block, 0,
+                         stream, p);
       break;
     default:
       return hipErrorInvalidValue;
@@ -828,6 +1073,13 @@ hipError_t launch_fa_fwd(int rule, int unit_rows, const FwdParams& p, int bh,
     else
       return hipErrorInvalidValue;
     return hipGetLastError();
+  }
+  if (p.qk_format == kQkMxfp8) {
+    // MX-FP8 Q K^T: 128-row decision units, ascending key order.
+    if (unit_rows != kTQ || p.key_order != kOrderAscending || p.q8 == nullptr ||
+        p.k8 == nullptr || p.q_scales == nullptr || p.k_scales == nullptr)
+      return hipErrorInvalidValue;
+    return launch_unit<kTQ, kOrderAscending, true>(rule, p, grid, stream);
   }
   if (unit_rows == kTQ) return launch_order<kTQ>(rule, p, grid, stream);
   if (unit_rows == 32) return launch_order<32>(rule, p, grid, stream);

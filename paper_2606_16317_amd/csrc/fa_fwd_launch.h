@@ -9,6 +9,7 @@ namespace dsattn {
 
 enum { kRuleDense = 0, kRuleBlasst = 1, kRuleDynSparse = 2, kRuleMask = 3 };
 enum { kOrderAscending = 0, kOrderDiagonal = 1 };
+enum { kQkBf16 = 0, kQkMxfp8 = 1 };
 
 struct FwdParams {
   const uint16_t* q;   // bf16 [BH][N][128]
@@ -26,6 +27,11 @@ struct FwdParams {
   float* lse;          // [BH][N] or null
   int key_order;       // kOrderAscending or kOrderDiagonal
   const uint8_t* mask_in;  // kRuleMask: [BH][n_qu][n_kt], 1 = skip (else unused)
+  int qk_format;           // kQkBf16 (q, k) or kQkMxfp8 (q8, k8 and their exponents)
+  const uint8_t* q8;       // kQkMxfp8: E4M3 codes [BH][N][128]
+  const uint8_t* k8;
+  const uint8_t* q_scales; // kQkMxfp8: E8M0 exponents [BH][N][4]
+  const uint8_t* k_scales;
 };
 
 // Enqueue one forward pass over `bh` heads on `stream`; unit_rows (128 or 32) is the

@@ -282,3 +282,32 @@ def test_quantize_rejects_host_pointers_and_accepts_empty():
     assert rc == -1 and "device pointer" in err
     rc, err = _call_raw("dsattn_quantize_mxfp8", None, None, None, 0, 128, None)
     assert rc == 0 and err == ""
+
+
+def test_qk_format_argument_checks():
+    pkg = _lib()
+    L = pkg.lib()
+
+    def call(**kw):
+        a = pkg.DsAttnArgs(pkg.RULE_DYNSPARSE_LAMBDA, -6.0, None, None, None, None, 1, 1, 256,
+                           128, 0.1, 128, 64, None, None, None, None, 0, None, pkg.QK_MXFP8,
+                           None, None)
+        for key, val in kw.items():
+            setattr(a, key, val)
+        return L.dsattn_attn_fwd_ex(ctypes.byref(a)), pkg.last_error()
+
+    assert call(qk_format=7) == (-1, "unknown qk format 7")
+    rc, err = call(tile_q=32)
+    assert rc == -2 and "tile_q = 128" in err
+    rc, err = call(key_order=pkg.ORDER_DIAGONAL)
+    assert rc == -2 and "ascending" in err
+    rc, err = call(rule=pkg.RULE_MASK)
+    assert rc == -2 and "bf16" in err
+    rc, err = call()
+    assert rc == -1 and "non-null" in err
+    assert call(N=0) == (0, "")
+    a = pkg.DsAttnArgs(pkg.RULE_DENSE, 0.0, None, None, None, None, 1, 1, 256, 128, 0.1, 128,
+                       64, None, None, None, None, 0, None, pkg.QK_MXFP8, None, None)
+    ws = (ctypes.c_uint8 * 256)()
+    assert L.dsattn_attn_fwd_reordered(ctypes.byref(a), None, None, ws, 256) == -2
+    assert "bf16" in pkg.last_error()

@@ -1,21 +1,28 @@
-"""GPU parity of the MX-FP8 quantisation kernel, called through the C ABI, against the
-CPU oracle (``oracle.mxfp8``): codes and block exponents must match bit for bit.
+"""GPU parity of the MX-FP8 path, called through the C ABI, against the CPU oracle.
 
-The inputs mix Gaussian rows of several scales, all-zero blocks, bf16 subnormals, the
-largest bf16 magnitudes, values exactly halfway between two E4M3 codes after scaling,
-and blocks whose scaled maximum rounds up to the saturation limit.
+* Quantisation (``dsattn_quantize_mxfp8``) against ``oracle.mxfp8``: codes and block
+  exponents must match bit for bit.  The inputs mix Gaussian rows of several scales,
+  all-zero blocks, bf16 subnormals, the largest bf16 magnitudes, values exactly halfway
+  between two E4M3 codes after scaling, and blocks whose scaled maximum rounds up to the
+  saturation limit.
+* Attention with MX-FP8 Q and K (DSATTN_QK_MXFP8) against the oracle run on the
+  dequantised Q and K (exact float64 values of the codes): the same teacher-forced
+  comparison and tolerances as the bf16 path, since S differs from the oracle's only by
+  the fp32 rounding of the MFMA sums.
 """
 
+import math
 import sys
 
 import numpy as np
 import pytest
 
 from oracle import bf16_to_f64
-from oracle.mxfp8 import quantize_mxfp8
+from oracle.mxfp8 import dequantize_mxfp8, quantize_mxfp8
 from synth import bf16_bits, make_random_qkv
 
-from _parity import to_device
+from _parity import (GpuRun, RULE_NAMES, assert_parity, compare, expected_stats_from_mask,
+                     from_device_bf16, sample_tiles, to_device)
 
 pytestmark = pytest.mark.gpu
 
@@ -98,3 +105,124 @@ def test_quantize_empty_and_row_len_32():
     want_c, want_s = quantize_mxfp8(bf16_to_f64(bits))
     np.testing.assert_array_equal(scales, want_s)
     np.testing.assert_array_equal(codes, want_c)
+
+
+# ---- attention with MX-FP8 Q and K --------------------------------------------------------
+
+SCALE = 1.0 / math.sqrt(128)
+
+
+def quantised(q, k):
+    """Oracle quantisation of bf16 q, k: (codes, exponents) of each and the dequantised
+    float64 values the oracle attends with."""
+    qc, qs = quantize_mxfp8(bf16_to_f64(q))
+    kc, ks = quantize_mxfp8(bf16_to_f64(k))
+    return (qc, qs, kc, ks), (dequantize_mxfp8(qc, qs), dequantize_mxfp8(kc, ks))
+
+
+def run_gpu_q8(qc, qs, kc, ks, vd, rule, param, scale=SCALE):
+    import torch
+    import paper_2606_16317_amd as dsa
+
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    B, H, N, d = vd.shape
+    n_qt, n_kt = -(-N // 128), -(-N // 64)
+    o = torch.empty_like(vd)
+    stats = torch.full((B * H * 4,), -7, dtype=torch.int64, device=vd.device)
+    mask = torch.full((B * H * n_qt * n_kt,), 7, dtype=torch.uint8, device=vd.device)
+    lse = torch.full((B * H * N,), float("nan"), dtype=torch.float32, device=vd.device)
+    args = [dev(a) if isinstance(a, np.ndarray) else a for a in (qc, qs, kc, ks)]
+    dsa.dsattn_attn_fwd_mxfp8(RULE_NAMES[rule], param, *args, vd, o, scale=scale,
+                              stats_out=stats, mask_out=mask, lse_out=lse)
+    torch.cuda.synchronize()
+    return GpuRun(from_device_bf16(o), mask.cpu().numpy().reshape(B, H, n_qt, n_kt),
+                  lse.cpu().numpy().reshape(B, H, N), stats.cpu().numpy().reshape(B, H, 4))
+
+
+Q8_RULES = [("dense", 0.0), ("dynsparse_lambda", -3.0), ("dynsparse_lambda", -6.0),
+            ("dynsparse_recall", 0.95), ("blasst", 0.05)]
+
+
+@pytest.mark.parametrize("B,H,N", [(1, 1, 1), (1, 1, 64), (1, 1, 65), (2, 3, 129),
+                                   (1, 2, 1000), (1, 1, 2047)])
+@pytest.mark.parametrize("rule,param", Q8_RULES)
+def test_q8_attention_ragged(B, H, N, rule, param):
+    q, k, v = make_random_qkv(B, H, N, 128, 7000 + 100 * B + 10 * H + N, q_std=1.5, k_std=1.5)
+    announce(f"q8 attention B={B} H={H} N={N} rule={rule} param={param}")
+    codes, (qf, kf) = quantised(q, k)
+    g = run_gpu_q8(*codes, to_device(v), rule, param)
+    rep = compare(qf, kf, v, g, rule, param, SCALE)
+    print(rep, flush=True)
+    assert_parity(rep)
+    assert (g.stats == expected_stats_from_mask(g.mask, N)).all()
+    assert not np.isnan(g.lse).any()
+
+
+@pytest.fixture(scope="module")
+def peaked_q8():
+    from synth import make_video_qkv
+
+    q, k, v, _ = make_video_qkv(1, 4, (2, 16, 32), 6.0, 6.0, True, 31)
+    codes, deq = quantised(q, k)
+    return (q, k, v), codes, deq, to_device(v)
+
+
+@pytest.mark.parametrize("rule,param", [("dynsparse_lambda", -6.0), ("dynsparse_recall", 0.9),
+                                        ("blasst", 1e-2)])
+def test_q8_attention_concentrated_heads_skip(peaked_q8, rule, param):
+    (q, k, v), codes, (qf, kf), vd = peaked_q8
+    announce(f"q8 peaked a=6 rule={rule} param={param}")
+    g = run_gpu_q8(*codes, vd, rule, param)
+    rep = compare(qf, kf, v, g, rule, param, SCALE,
+                  tiles=sample_tiles(1, 4, q.shape[2], per_head=4, seed=3))
+    print(rep, flush=True)
+    assert_parity(rep)
+    assert rep.sparsity > 0.1
+    assert (g.stats == expected_stats_from_mask(g.mask, q.shape[2])).all()
+
+
+def test_q8_attention_from_gpu_quantisation_is_identical():
+    """Quantising on the GPU and attending gives the same bits as attending with the
+    oracle's codes (the quantiser is bit-exact), and a second run repeats them."""
+    import paper_2606_16317_amd as dsa
+
+    announce("q8 pipeline N=1000 H=2 lambda=-4")
+    q, k, v = make_random_qkv(1, 2, 1000, 128, 77, q_std=2.0, k_std=2.0)
+    codes, _ = quantised(q, k)
+    vd = to_device(v)
+    a = run_gpu_q8(*codes, vd, "dynsparse_lambda", -4.0)
+    qc, qs = dsa.dsattn_quantize_mxfp8(to_device(q))
+    kc, ks = dsa.dsattn_quantize_mxfp8(to_device(k))
+    b = run_gpu_q8(qc, qs, kc, ks, vd, "dynsparse_lambda", -4.0)
+    c = run_gpu_q8(qc, qs, kc, ks, vd, "dynsparse_lambda", -4.0)
+    for x in (b, c):
+        np.testing.assert_array_equal(x.o, a.o)
+        np.testing.assert_array_equal(x.mask, a.mask)
+        np.testing.assert_array_equal(x.lse, a.lse)
+
+
+def test_q8_attention_close_to_bf16_attention():
+    """The difference between the dense outputs of the MX-FP8 and bf16 paths is the
+    quantisation error the oracle predicts (fp64 attention on dequantised vs bf16 Q, K):
+    the GPU's relative L2 difference lies within 10 % of the oracle's."""
+    import paper_2606_16317_amd as dsa
+
+    announce("q8 vs bf16 dense N=1024 H=2")
+    q, k, v = make_random_qkv(1, 2, 1024, 128, 78)
+    codes, (qf, kf) = quantised(q, k)
+    vd = to_device(v)
+    a = bf16_to_f64(run_gpu_q8(*codes, vd, "dense", 0.0).o)
+    b = bf16_to_f64(from_device_bf16(dsa.dense_attn_fwd(to_device(q), to_device(k), vd)))
+
+    def attend(qq, kk, vv):
+        s = SCALE * (qq @ kk.T)
+        p = np.exp(s - s.max(axis=1, keepdims=True))
+        return (p / p.sum(axis=1, keepdims=True)) @ vv
+
+    for h in range(2):
+        vv = bf16_to_f64(v[0, h])
+        exact = attend(bf16_to_f64(q[0, h]), bf16_to_f64(k[0, h]), vv)
+        quant = attend(qf[0, h], kf[0, h], vv)
+        want = np.linalg.norm(quant - exact) / np.linalg.norm(exact)
+        got = np.linalg.norm(a[0, h] - b[0, h]) / np.linalg.norm(b[0, h])
+        assert abs(got - want) < 0.1 * want, (h, got, want)
