@@ -16,8 +16,9 @@ the spatio-temporally blocked token order (``dsattn_attn_fwd_reordered``, gather
 output scatter included in its time), plus the HBM rate of the row gather kernel;
 ``--reuse-sweep`` times a DynSparse call that writes its skip mask, then the mask-reuse call
 (DSATTN_RULE_MASK) that applies that mask, per threshold and decision unit;
-``--q8-sweep`` times the MX-FP8 quantisation of Q and K, then per rule/threshold the bf16
-call next to the call with MX-FP8 Q and K (DSATTN_QK_MXFP8).
+``--q8-sweep`` times the MX-FP8 quantisation of Q and K (and the key mean and shifted
+quantisation of key smoothing), then per rule/threshold the bf16 call next to the call with
+MX-FP8 Q and K (DSATTN_QK_MXFP8), with plain and with smoothed keys.
 """
 
 from __future__ import annotations
@@ -481,6 +482,24 @@ def q8_sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop):
                                    "frac": moved / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}}),
           flush=True)
     dsa.dsattn_quantize_mxfp8(kd, kc, ks)
+    # key smoothing: the per-head mean key, then K - mean quantised
+    mean = torch.empty((B, H, D), dtype=torch.float32, device="cuda")
+    ms = time_calls(lambda: dsa.dsattn_key_mean(kd, mean), args.steps, args.warmup)
+    moved = B * H * N * D * 2 + B * H * D * 4
+    print(json.dumps({"workload": w.name, "kernel": "key_mean", "ms": ms,
+                      "roofline": {"bound": "hbm", "achieved": moved / (ms * 1e-3) / 1e9,
+                                   "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                   "frac": moved / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}}),
+          flush=True)
+    kcs, kss = torch.empty_like(kc), torch.empty_like(ks)
+    ms = time_calls(lambda: dsa.dsattn_quantize_mxfp8(kd, kcs, kss, shift=mean), args.steps,
+                    args.warmup)
+    moved = B * H * N * (2 * D + D + D // 32) + B * H * D * 4
+    print(json.dumps({"workload": w.name, "kernel": "quantize_mxfp8_shift", "ms": ms,
+                      "roofline": {"bound": "hbm", "achieved": moved / (ms * 1e-3) / 1e9,
+                                   "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                   "frac": moved / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}}),
+          flush=True)
     rules = {"dense": dsa.RULE_DENSE, "dynsparse_recall": dsa.RULE_DYNSPARSE_RECALL,
              "dynsparse_lambda": dsa.RULE_DYNSPARSE_LAMBDA, "blasst": dsa.RULE_BLASST}
     points = [("dense", 0.0), ("dynsparse_recall", 0.95), ("dynsparse_lambda", -10.0),
@@ -488,13 +507,14 @@ def q8_sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop):
     dense_ms = None
     for rule, p in points:
         rec = {"workload": w.name, "rule": rule, "param": p}
-        for fmt in ("bf16", "mxfp8"):
+        for fmt in ("bf16", "mxfp8", "mxfp8_smooth"):
             out = od if (rule == "dense" and fmt == "bf16") else o
             if fmt == "bf16":
                 fn = lambda: dsa.dsattn_attn_fwd_ex(rules[rule], p, qd, kd, vd, out, scale=scale,
                                                     stats_out=stats)
             else:
-                fn = lambda: dsa.dsattn_attn_fwd_mxfp8(rules[rule], p, qc, qs, kc, ks, vd, out,
+                kk, kks = (kc, ks) if fmt == "mxfp8" else (kcs, kss)
+                fn = lambda: dsa.dsattn_attn_fwd_mxfp8(rules[rule], p, qc, qs, kk, kks, vd, out,
                                                        scale=scale, stats_out=stats)
             print(f"[q8-sweep] {rule} {p} {fmt}", file=sys.stderr, flush=True)
             ms = time_calls(fn, args.steps, args.warmup)
@@ -507,7 +527,7 @@ def q8_sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop):
             qk, pv = 2 * D * elems, 2 * D * (elems - skipped)
             # time the issued MFMA work needs at peak: Q K^T at the fp8 (or bf16) rate, P V
             # at the bf16 rate
-            t_min = qk / ((PEAK_FP8_TFLOPS if fmt == "mxfp8" else PEAK_BF16_TFLOPS) * 1e12) + \
+            t_min = qk / ((PEAK_BF16_TFLOPS if fmt == "bf16" else PEAK_FP8_TFLOPS) * 1e12) + \
                 pv / (PEAK_BF16_TFLOPS * 1e12)
             rec[fmt] = {"ms": ms, "effective_tflops": dense_flop / (ms * 1e-3) / 1e12,
                         "sparsity_tiles": float(st[:, 1].sum() / st[:, 0].sum()),

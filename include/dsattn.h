@@ -253,6 +253,30 @@ int dsattn_attn_fwd_reordered(const dsattn_args* args, const int32_t* q_index,
 int dsattn_quantize_mxfp8(const void* src, void* codes, void* scales, long long rows,
                           int row_len, hipStream_t stream);
 
+/*
+ * Key smoothing for the quantised path.  Subtracting one vector m from every key of a head
+ * shifts all scores of a query row by the same -q.m, which the softmax removes: the
+ * attention output and the rule's decisions (they compare score differences) are
+ * unchanged in exact arithmetic, while keys that share a large common component quantise
+ * with a much smaller error once it is removed.  The LSE of the smoothed scores is the
+ * original one minus scale * q.m.
+ *
+ * dsattn_key_mean: mean_out[h][c] = (1/N) sum_n k[h][n][c] in float32 for BH heads of N
+ * bf16 keys of d values (d a power of two in [8, 1024]; k 16-byte aligned, mean_out 4-byte
+ * aligned, both device pointers).  The summation order is fixed, so repeated calls give
+ * the same bits.  N must be > 0 when BH > 0.
+ *
+ * dsattn_quantize_mxfp8_shift: as dsattn_quantize_mxfp8 on the float32 values
+ * x - shift[i / group_rows][c] (each difference rounded to nearest float32) for element c
+ * of row i; shift is a 16-byte aligned device array of float32 [ceil(rows/group_rows)]
+ * [row_len].  For keys [B][H][N][d] and the mean of dsattn_key_mean, group_rows = N.
+ * x - shift must stay finite.
+ */
+int dsattn_key_mean(const void* k, float* mean_out, int BH, int N, int d, hipStream_t stream);
+int dsattn_quantize_mxfp8_shift(const void* src, const float* shift, void* codes, void* scales,
+                                long long rows, int row_len, long long group_rows,
+                                hipStream_t stream);
+
 /* Message describing the last error on this thread ("" after a successful call). */
 const char* dsattn_last_error(void);
 

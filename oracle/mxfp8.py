@@ -16,10 +16,21 @@ Quantisation of one block x[0..31] (as in the MX specification):
 * each element is x / 2^E rounded to the nearest E4M3 value, ties to the even code,
   magnitudes above 448 saturating to 448.
 
+Key smoothing (optional, before quantising K): subtracting one vector m from every key of
+a head adds the same constant -q.m to every score of a query row, which the softmax
+removes, so the attention output and every skip decision of the rule (which compares
+score differences only) are unchanged in exact arithmetic, while the keys lose their
+common component and quantise with a smaller relative error.  The natural choice of m is
+the mean key of the head; the subtraction is done in float32 (x - m rounded to nearest
+float32) and the result quantised as above.  The LSE of the smoothed scores is that of
+the original ones minus scale * q.m.
+
 This module finds the nearest E4M3 value by searching the table of all codes, which is a
 different route from the bit manipulation of the HIP kernel.  Parity status: pinned by
 ``tests/test_oracle_mxfp8.py`` (hand-worked blocks, exactly representable round trips,
-ties, saturation, subnormals, zero blocks, the decoded code table).
+ties, saturation, subnormals, zero blocks, the decoded code table; the key mean on
+constant and arithmetic-progression keys, the float32 rounding of the subtraction, and the
+invariance of the attention output and of the rule's decisions under smoothing).
 """
 
 from __future__ import annotations
@@ -102,3 +113,17 @@ def dequantize_mxfp8(codes: np.ndarray, scale_codes: np.ndarray) -> np.ndarray:
     vals = e4m3_decode(codes).reshape(*codes.shape[:-1], n // BLOCK, BLOCK)
     scale = np.ldexp(1.0, np.asarray(scale_codes, dtype=np.int64) - 127)
     return (vals * scale[..., None]).reshape(codes.shape)
+
+
+def key_mean(k: np.ndarray) -> np.ndarray:
+    """Mean key of every head: float64 [..., d] of k [..., N, d] (float values)."""
+    return np.asarray(k, dtype=np.float64).mean(axis=-2)
+
+
+def smooth_keys(k: np.ndarray, shift: np.ndarray) -> np.ndarray:
+    """float32 k - shift for every key of a head: k [..., N, d] (values exactly
+    representable in float32, e.g. bf16), shift [..., d] rounded to float32 first; each
+    difference is rounded to nearest float32, as the quantiser does."""
+    k32 = np.asarray(k, dtype=np.float64).astype(np.float32)
+    s32 = np.asarray(shift, dtype=np.float64).astype(np.float32)
+    return (k32 - s32[..., None, :]).astype(np.float32)

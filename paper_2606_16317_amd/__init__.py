@@ -111,6 +111,12 @@ def lib():
                                                                       ctypes.c_int,
                                                                       ctypes.c_void_p]
         L.dsattn_quantize_mxfp8.restype = ctypes.c_int
+        L.dsattn_quantize_mxfp8_shift.argtypes = [ctypes.c_void_p] * 4 + [
+            ctypes.c_longlong, ctypes.c_int, ctypes.c_longlong, ctypes.c_void_p]
+        L.dsattn_quantize_mxfp8_shift.restype = ctypes.c_int
+        L.dsattn_key_mean.argtypes = [ctypes.c_void_p, ctypes.c_void_p] + [ctypes.c_int] * 3 + [
+            ctypes.c_void_p]
+        L.dsattn_key_mean.restype = ctypes.c_int
         L.dsattn_last_error.argtypes = []
         L.dsattn_last_error.restype = ctypes.c_char_p
         L.dsattn_version.argtypes = []
@@ -341,9 +347,11 @@ def dsattn_scatter_rows(src, index, dst=None, stream=None):
     return dst
 
 
-def dsattn_quantize_mxfp8(x, codes=None, scales=None, stream=None):
+def dsattn_quantize_mxfp8(x, codes=None, scales=None, shift=None, stream=None):
     """MX-FP8 codes (uint8, like x) and E8M0 block scales (uint8 [..., n / 32]) of a
-    contiguous bf16 GPU tensor whose last axis is a multiple of 32."""
+    contiguous bf16 GPU tensor whose last axis is a multiple of 32.  With ``shift`` (float32
+    [B, H, n] for x [B, H, N, n], e.g. from ``dsattn_key_mean``) every row first has its
+    head's vector subtracted (key smoothing)."""
     import torch
 
     if x.dtype != torch.bfloat16 or not x.is_cuda or not x.is_contiguous():
@@ -353,10 +361,33 @@ def dsattn_quantize_mxfp8(x, codes=None, scales=None, stream=None):
     codes = torch.empty(x.shape, dtype=torch.uint8, device=x.device) if codes is None else codes
     if scales is None:
         scales = torch.empty((*x.shape[:-1], n // 32), dtype=torch.uint8, device=x.device)
-    rc = lib().dsattn_quantize_mxfp8(x.data_ptr(), codes.data_ptr(), scales.data_ptr(), rows, n,
-                                     _stream(stream))
-    _check(rc, "dsattn_quantize_mxfp8")
+    if shift is None:
+        rc = lib().dsattn_quantize_mxfp8(x.data_ptr(), codes.data_ptr(), scales.data_ptr(), rows,
+                                         n, _stream(stream))
+        _check(rc, "dsattn_quantize_mxfp8")
+        return codes, scales
+    if x.dim() != 4 or tuple(shift.shape) != (x.shape[0], x.shape[1], n) or \
+            shift.dtype != torch.float32 or not shift.is_cuda or not shift.is_contiguous():
+        raise ValueError("shift must be a contiguous float32 GPU tensor [B, H, n] for x [B, H, N, n]")
+    rc = lib().dsattn_quantize_mxfp8_shift(x.data_ptr(), shift.data_ptr(), codes.data_ptr(),
+                                           scales.data_ptr(), rows, n, int(x.shape[2]),
+                                           _stream(stream))
+    _check(rc, "dsattn_quantize_mxfp8_shift")
     return codes, scales
+
+
+def dsattn_key_mean(k, out=None, stream=None):
+    """Mean key of every head: float32 [B, H, d] of a contiguous bf16 GPU tensor
+    [B, H, N, d] (fixed summation order)."""
+    import torch
+
+    if k.dtype != torch.bfloat16 or not k.is_cuda or not k.is_contiguous() or k.dim() != 4:
+        raise ValueError("k must be a contiguous bf16 GPU tensor [B, H, N, d]")
+    B, H, N, d = (int(x) for x in k.shape)
+    out = torch.empty((B, H, d), dtype=torch.float32, device=k.device) if out is None else out
+    rc = lib().dsattn_key_mean(k.data_ptr(), out.data_ptr(), B * H, N, d, _stream(stream))
+    _check(rc, "dsattn_key_mean")
+    return out
 
 
 def dsattn_reordered_workspace_bytes(B, H, N, d=HEAD_DIM, with_lse=False):
@@ -398,5 +429,5 @@ __all__ = [
     "dynsparse_attn_fwd", "dynsparse_attn_fwd_lambda", "blasst_attn_fwd", "dense_attn_fwd",
     "dsattn_attn_fwd_ex", "dsattn_block_order", "dsattn_gather_rows", "dsattn_scatter_rows",
     "dsattn_reordered_workspace_bytes", "dsattn_attn_fwd_reordered", "dsattn_quantize_mxfp8",
-    "dsattn_attn_fwd_mxfp8", "QK_BF16", "QK_MXFP8",
+    "dsattn_attn_fwd_mxfp8", "dsattn_key_mean", "QK_BF16", "QK_MXFP8",
 ]

@@ -488,11 +488,15 @@ int dsattn_attn_fwd_reordered(const dsattn_args* args, const int32_t* q_index,
   return DSATTN_OK;
 }
 
-int dsattn_quantize_mxfp8(const void* src, void* codes, void* scales, long long rows,
-                          int row_len, hipStream_t stream) {
+namespace {
+
+int quantize(const void* src, const float* shift, void* codes, void* scales, long long rows,
+             int row_len, long long group_rows, hipStream_t stream) {
   if (rows < 0) return fail(DSATTN_EINVAL, "rows must be >= 0");
   if (row_len <= 0 || row_len % 32 != 0)
     return fail(DSATTN_EINVAL, "row_len must be a positive multiple of 32 (got %d)", row_len);
+  if (shift != nullptr && group_rows <= 0)
+    return fail(DSATTN_EINVAL, "group_rows must be > 0 (got %lld)", group_rows);
   const long long n_blocks = rows * (row_len / 32);
   if (rows > 0 && n_blocks / rows != row_len / 32) return fail(DSATTN_EINVAL, "problem too large");
   if (n_blocks > (1LL << 40)) return fail(DSATTN_EINVAL, "problem too large");
@@ -509,8 +513,47 @@ int dsattn_quantize_mxfp8(const void* src, void* codes, void* scales, long long 
   }
   if (!aligned(src, 16) || !aligned(codes, 16))
     return fail(DSATTN_EINVAL, "src and codes must be 16-byte aligned");
-  const hipError_t e = dsattn::launch_quantize_mxfp8(src, codes, scales, n_blocks, stream);
+  if (shift != nullptr && (!is_device_pointer(shift) || !aligned(shift, 16)))
+    return fail(DSATTN_EINVAL, "shift must be a 16-byte aligned device pointer");
+  const hipError_t e = dsattn::launch_quantize_mxfp8(src, codes, scales, n_blocks, shift,
+                                                     row_len / 32, group_rows, stream);
   if (e != hipSuccess) return fail(DSATTN_ELAUNCH, "quantize launch failed: %s", hipGetErrorString(e));
+  g_last_error.clear();
+  return DSATTN_OK;
+}
+
+}  // namespace
+
+int dsattn_quantize_mxfp8(const void* src, void* codes, void* scales, long long rows,
+                          int row_len, hipStream_t stream) {
+  return quantize(src, nullptr, codes, scales, rows, row_len, 1, stream);
+}
+
+int dsattn_quantize_mxfp8_shift(const void* src, const float* shift, void* codes, void* scales,
+                                long long rows, int row_len, long long group_rows,
+                                hipStream_t stream) {
+  if (shift == nullptr) return fail(DSATTN_EINVAL, "shift must be non-null");
+  return quantize(src, shift, codes, scales, rows, row_len, group_rows, stream);
+}
+
+int dsattn_key_mean(const void* k, float* mean_out, int BH, int N, int d, hipStream_t stream) {
+  if (BH < 0 || N < 0) return fail(DSATTN_EINVAL, "BH and N must be >= 0");
+  if (BH > 65535) return fail(DSATTN_EINVAL, "BH must be <= 65535 (got %d)", BH);
+  if (d < 8 || d > 1024 || (d & (d - 1)) != 0)
+    return fail(DSATTN_EINVAL, "d must be a power of two in [8, 1024] (got %d)", d);
+  if (N == 0 || BH == 0) {
+    if (N == 0 && BH > 0) return fail(DSATTN_EINVAL, "the mean of zero keys is undefined");
+    g_last_error.clear();
+    return DSATTN_OK;
+  }
+  if ((long long)N * d > (1LL << 31)) return fail(DSATTN_EINVAL, "N * d is too large for one head");
+  if (k == nullptr || mean_out == nullptr) return fail(DSATTN_EINVAL, "k and mean_out must be non-null");
+  if (!is_device_pointer(k) || !is_device_pointer(mean_out))
+    return fail(DSATTN_EINVAL, "k and mean_out must be device pointers");
+  if (!aligned(k, 16) || !aligned(mean_out, 4))
+    return fail(DSATTN_EINVAL, "k must be 16-byte and mean_out 4-byte aligned");
+  const hipError_t e = dsattn::launch_key_mean(k, mean_out, BH, N, d, stream);
+  if (e != hipSuccess) return fail(DSATTN_ELAUNCH, "key mean launch failed: %s", hipGetErrorString(e));
   g_last_error.clear();
   return DSATTN_OK;
 }

@@ -311,3 +311,29 @@ def test_qk_format_argument_checks():
     ws = (ctypes.c_uint8 * 256)()
     assert L.dsattn_attn_fwd_reordered(ctypes.byref(a), None, None, ws, 256) == -2
     assert "bf16" in pkg.last_error()
+
+
+@pytest.mark.parametrize("bh,n,d,msg", [
+    (-1, 4, 128, ">= 0"), (70000, 4, 128, "65535"), (1, 4, 96, "power of two"),
+    (1, 4, 4, "power of two"), (1, 4, 2048, "power of two"), (1, 0, 128, "zero keys"),
+    (1, 1 << 30, 128, "too large"), (1, 4, 128, "non-null"),
+])
+def test_key_mean_rejects_bad_arguments(bh, n, d, msg):
+    rc, err = _call_raw("dsattn_key_mean", None, None, bh, n, d, None)
+    assert rc == -1 and msg in err
+
+
+def test_key_mean_and_shifted_quantize_host_checks():
+    buf = (ctypes.c_uint32 * 64)()
+    p = ctypes.addressof(buf)
+    rc, err = _call_raw("dsattn_key_mean", p, p, 1, 4, 128, None)
+    assert rc == -1 and "device pointers" in err
+    assert _call_raw("dsattn_key_mean", None, None, 0, 4, 128, None) == (0, "")
+    rc, err = _call_raw("dsattn_quantize_mxfp8_shift", None, None, None, None, 4, 128, 4, None)
+    assert rc == -1 and "shift must be non-null" in err
+    rc, err = _call_raw("dsattn_quantize_mxfp8_shift", None, p, None, None, 4, 128, 0, None)
+    assert rc == -1 and "group_rows" in err
+    rc, err = _call_raw("dsattn_quantize_mxfp8_shift", None, p, None, None, 4, 100, 4, None)
+    assert rc == -1 and "multiple of 32" in err
+    rc, err = _call_raw("dsattn_quantize_mxfp8_shift", None, p, None, None, 0, 128, 4, None)
+    assert rc == 0 and err == ""

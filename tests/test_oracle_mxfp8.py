@@ -123,3 +123,69 @@ def test_rule_attention_accepts_dequantised_inputs():
     for ra, rb in zip(a.results, b.results):
         assert np.array_equal(ra.skip, rb.skip)
         np.testing.assert_array_equal(ra.o_sparse, rb.o_sparse)
+
+
+def test_key_mean_closed_forms():
+    from oracle.mxfp8 import key_mean
+
+    k = np.zeros((2, 3, 100, 8))
+    k[0, 1] = 2.5                                   # constant keys: the constant
+    k[1, 2, :, 3] = np.arange(100)                  # 0..99: mean 49.5
+    k[1, 0, :, 0] = np.where(np.arange(100) % 2, 1.0, -3.0)   # alternating: -1
+    m = key_mean(k)
+    assert m.shape == (2, 3, 8)
+    assert (m[0, 1] == 2.5).all() and (m[0, 0] == 0).all()
+    assert m[1, 2, 3] == 49.5 and m[1, 0, 0] == -1.0
+
+
+def test_smooth_keys_rounds_each_difference_to_float32():
+    from oracle.mxfp8 import smooth_keys
+
+    k = np.array([[[1.5, 1.0, 3.0e38]]])
+    sh = np.array([[0.25, 2.0 ** -30, -1.0]])
+    out = smooth_keys(k, sh)
+    assert out.dtype == np.float32
+    assert out[0, 0, 0] == 1.25                     # exact
+    assert out[0, 0, 1] == np.float32(1.0)          # 1 - 2^-30 rounds back to 1 in float32
+    assert out[0, 0, 2] == np.float32(3.0e38)       # 3e38 + 1 rounds to 3e38
+
+
+def test_smoothing_leaves_output_and_decisions_unchanged():
+    """Subtracting the mean key shifts every score of a row by one constant: in exact
+    arithmetic the output and the rule's decisions do not move.  In float64 the outputs
+    agree to rounding and every decision with a margin above rounding is the same."""
+    import oracle
+    from oracle.mxfp8 import key_mean, smooth_keys
+    from synth import make_video_qkv
+
+    q, k, v, _ = make_video_qkv(1, 2, (2, 8, 32), 4.0, 4.0, True, 12)
+    kf = oracle.bf16_to_f64(k)
+    ks = smooth_keys(kf, key_mean(kf)).astype(np.float64)
+    assert np.abs(key_mean(ks)).max() < 1e-3 * np.abs(kf).max()   # common part removed
+    a = oracle.rule_attention(q, kf, v, 0.088, "dynsparse", -6.0, 128, 64)
+    b = oracle.rule_attention(q, ks, v, 0.088, "dynsparse", -6.0, 128, 64)
+    skipped = 0
+    for ra, rb in zip(a.results, b.results):
+        sure = np.abs(ra.margin) > 1e-9
+        assert np.array_equal(ra.skip[sure], rb.skip[sure])
+        skipped += int(ra.skip.sum())
+        if np.array_equal(ra.skip, rb.skip):
+            np.testing.assert_allclose(rb.o_sparse, ra.o_sparse, rtol=0, atol=1e-6)
+    assert skipped > 0
+
+
+def test_smoothing_reduces_the_quantisation_error_of_a_common_key_component():
+    """Keys with a large shared component quantise with a large error relative to their
+    spread; after smoothing the error on the scores is several times smaller."""
+    from oracle.mxfp8 import key_mean, smooth_keys
+
+    rng = np.random.default_rng(9)
+    k = 8.0 + rng.normal(0, 1, (1, 1, 512, 128))      # common part 8, spread 1
+    q = rng.normal(0, 1, (64, 128))
+    s = q @ k[0, 0].T
+    m = key_mean(k)
+    s_plain = q @ dequantize_mxfp8(*quantize_mxfp8(k))[0, 0].T
+    ks = smooth_keys(k, m).astype(np.float64)
+    s_smooth = q @ dequantize_mxfp8(*quantize_mxfp8(ks))[0, 0].T + (q @ m[0, 0].astype(np.float32))[:, None]
+    err = lambda x: np.sqrt(((x - s) ** 2).mean())
+    assert err(s_smooth) * 4 < err(s_plain)
