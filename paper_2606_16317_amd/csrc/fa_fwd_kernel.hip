@@ -25,7 +25,7 @@
 //
 // Pipeline (one barrier per key tile): S_{j+1} is computed during iteration j, so the
 // decision for tile j+1 is voted before the barrier that closes iteration j and read
-// right after it.  K is prefetched two tiles ahead and V one tile ahead, straight from
+// right after it (the read's latency overlaps the issue of the next K-tile DMA).  K is prefetched two tiles ahead and V one tile ahead, straight from
 // global memory into LDS (buffer loads with the LDS bit; rows past the sequence end come
 // back as zeros from the buffer range check); V is fetched only for tiles that follow a
 // kept tile or are themselves kept, so runs of skipped tiles stream K alone.  Inside an iteration the instruction
@@ -588,10 +588,13 @@ __device__ __forceinline__ void load_k_tile(Smem& sm, int buf, const LoopCtx& cx
 }
 
 // One loop step j, visiting key tile key_tile_at(j) (written "tile j" below; LDS buffers
-// rotate with the step).  On entry s_cur holds S_j, mhat its row max (log2 units), keep_own
-// the decision for tile j of this wave's decision unit (the workgroup's 128 query rows,
-// or with UNIT = 32 the wave's own rows), keep_any whether any unit of the workgroup keeps
-// tile j, and v_ready whether V_j is already in LDS (buffer j % 2).  On exit s_next holds
+// rotate with the step).  On entry s_cur holds S_j, mhat its row max (log2 units), vote the
+// workgroup's vote word for tile j (one byte per wave, loaded after the last barrier and
+// read only once the next K tile's DMA is out, so that the LDS latency overlaps it),
+// keep_own the decision for tile j of this wave's decision unit when that unit is the
+// wave's own 32 rows (UNIT = 32; with the workgroup's 128 rows it comes from the vote),
+// and v_ready whether V_j is already in LDS (buffer j % 2).  keep_any (some unit of the
+// workgroup keeps tile j) is set from the vote.  On exit s_next holds
 // S_{j+1}, the other state refers to tile j+1, and every wave has passed the barrier that
 // publishes K_{j+2}, the V_{j+1} buffer if it was requested, and the tile-(j+1) votes.
 //
@@ -602,7 +605,8 @@ __device__ __forceinline__ void load_k_tile(Smem& sm, int buf, const LoopCtx& cx
 template <int RULE, int UNIT, int ORDER, bool Q8>
 __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f32x16 (&s_next)[2],
                                               float& mhat, bool& keep_own, bool& keep_any,
-                                              bool& v_ready, RowState& rs, f32x16 (&o)[4],
+                                              uint32_t& vote, bool& v_ready, RowState& rs,
+                                              f32x16 (&o)[4],
                                               const typename QFragOf<Q8>::type& qf, Smem& sm,
                                               const LoopCtx& cx, SkipCount& sk) {
   const int nb = (j + 1) & 1;
@@ -610,6 +614,13 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
   const int tj = key_tile_at<ORDER>(j, cx);          // key tiles of steps j, j+1, j+2
   const int tn = key_tile_or_past<ORDER>(j + 1, cx);
   const int tn2 = key_tile_or_past<ORDER>(j + 2, cx);
+  // The K tile two steps ahead does not depend on the decision: its DMA goes out while the
+  // vote word read after the last barrier is still in flight.
+  load_k_tile<Q8>(sm, j & 1, cx, tn2 * kTK);
+  if constexpr (RULE != kRuleDense) {
+    keep_any = __builtin_amdgcn_readfirstlane(vote) != 0;
+    if constexpr (UNIT == kTQ) keep_own = keep_any;
+  }
   if (cx.mask_row != nullptr && (UNIT == kTQ ? cx.w == 0 : true) && cx.lane == 0)
     cx.mask_row[tj] = keep_own ? 0 : 1;
 
@@ -624,7 +635,6 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
     asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
   }
   if (keep_any) load_tile_lds(sm.v[nb], cx.vrs, cx.voff, tn * kTK, cx.w);
-  load_k_tile<Q8>(sm, j & 1, cx, tn2 * kTK);
 
   // S_{j+1} is computed on both paths (on the last tile it reads a stale buffer and is
   // dropped).
@@ -662,9 +672,8 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
   if (has_next) {
     if constexpr (RULE != kRuleDense) {
-      keep_any = __builtin_amdgcn_readfirstlane(
-                     *reinterpret_cast<const uint32_t*>(sm.vote[nb])) != 0;
-      keep_own = UNIT == kTQ ? keep_any : wave_keeps;
+      vote = *reinterpret_cast<const uint32_t*>(sm.vote[nb]);   // consumed by the next step
+      if constexpr (UNIT != kTQ) keep_own = wave_keeps;
     }
     mhat = mhat_next;
   }
@@ -788,17 +797,18 @@ fa_fwd_kernel(FwdParams p) {
   float mhat = row_max(sa) * cx.c;
   bool keep_own = true;                      // the first tile is always kept
   bool keep_any = true;
+  uint32_t vote = 1;                         // the first tile's "vote": kept
   bool v_ready = true;                       // V_0 was staged above
   SkipCount sk;
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");  // K_0 consumed
 
   // Unrolled by two so that S_j / S_{j+1} alternate between sa and sb without copies.
   for (int j = 0; j < cx.n_kt; j += 2) {
-    key_tile_step<RULE, UNIT, ORDER, Q8>(j, sa, sb, mhat, keep_own, keep_any, v_ready, rs, o,
-                                         qf, sm, cx, sk);
+    key_tile_step<RULE, UNIT, ORDER, Q8>(j, sa, sb, mhat, keep_own, keep_any, vote, v_ready, rs,
+                                         o, qf, sm, cx, sk);
     if (j + 1 < cx.n_kt)
-      key_tile_step<RULE, UNIT, ORDER, Q8>(j + 1, sb, sa, mhat, keep_own, keep_any, v_ready, rs,
-                                           o, qf, sm, cx, sk);
+      key_tile_step<RULE, UNIT, ORDER, Q8>(j + 1, sb, sa, mhat, keep_own, keep_any, vote,
+                                           v_ready, rs, o, qf, sm, cx, sk);
   }
 
   store_rows(p, o, rs, cx, head_off, bh, qrow);
