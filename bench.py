@@ -27,6 +27,7 @@ import argparse
 import json
 import math
 import os
+import re
 import sys
 import time
 
@@ -201,7 +202,8 @@ def traffic_summary(fetch_dir, write_dir, workload, command):
             if r["Counter_Name"] != counter:
                 continue
             kib = float(r["Counter_Value"])
-            if "fa_fwd_kernel<2>" in r["Kernel_Name"]:
+            # DynSparse rule, 128-row units, ascending order, bf16 Q and K
+            if re.search(r"fa_fwd_kernel<2, 128, 0, false>", r["Kernel_Name"]):
                 vals["main"].append(kib)
             elif "AUnaryFunctor" in r["Kernel_Name"] or "MulFunctor" in r["Kernel_Name"]:
                 vals["copy"].append(kib)
