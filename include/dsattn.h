@@ -170,8 +170,8 @@ int dsattn_attn_fwd_ex(const dsattn_args* args);
  */
 
 /*
- * Quantised Q K^T (DSATTN_QK_MXFP8; Section 1 lists quantised attention among the methods
- * the rule combines with).  q and k then point at E4M3 codes (uint8 [B][H][N][d], 16-byte
+ * Quantised Q K^T (DSATTN_QK_MXFP8; the Conclusion, Section 5, lists quantisation among
+ * the methods the rule combines with).  q and k then point at E4M3 codes (uint8 [B][H][N][d], 16-byte
  * aligned) and q_scales / k_scales at their E8M0 block exponents (uint8 [B][H][N][d/32],
  * 4-byte aligned), as written by dsattn_quantize_mxfp8: element x of block b of a row
  * stands for e4m3(x) * 2^(scale[b] - 127).  S = Q K^T is computed from these values with
@@ -240,8 +240,8 @@ int dsattn_attn_fwd_reordered(const dsattn_args* args, const int32_t* q_index,
                               size_t workspace_bytes);
 
 /*
- * MX-FP8 quantisation of bf16 rows, the storage of the quantised Q K^T variant (Section 1
- * lists quantised attention among the methods the rule combines with).  src holds `rows`
+ * MX-FP8 quantisation of bf16 rows, the storage of the quantised Q K^T variant (the
+ * Conclusion, Section 5, lists quantisation among the methods the rule combines with).  src holds `rows`
  * rows of `row_len` bf16 values (row_len a multiple of 32); every 32 consecutive values
  * of a row form a block that shares the scale 2^E, E = floor(log2(max |x|)) - 8, written
  * to `scales` as the E8M0 code E + 127 (uint8 [rows][row_len / 32]; 0 for an all-zero

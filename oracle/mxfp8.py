@@ -2,7 +2,7 @@
 
 TEST INFRASTRUCTURE ONLY (same rule as the rest of ``oracle/``).
 
-Section 1 lists quantised attention among the methods DynSparse combines with.  The
+The Conclusion (Section 5) lists quantisation among the methods DynSparse combines with.  The
 quantised variant here stores Q and K in the OCP Microscaling (MX) FP8 format: every run of
 32 consecutive values of a row (a block along the head dimension) shares one power-of-two
 scale stored as an E8M0 exponent, and each value is an FP8 E4M3 number (1 sign bit, 4

@@ -1,5 +1,5 @@
-// MX-FP8 quantisation of bf16 rows (the storage of a quantised Q K^T; Section 1 lists
-// quantised attention among the methods the rule combines with), optionally of rows minus
+// MX-FP8 quantisation of bf16 rows (the storage of a quantised Q K^T; the Conclusion,
+// Section 5, lists quantisation among the methods the rule combines with), optionally of rows minus
 // a float32 shift vector (key smoothing), and the per-head mean key that serves as that
 // shift.
 //
