@@ -176,8 +176,9 @@ int dsattn_attn_fwd_ex(const dsattn_args* args);
  * 4-byte aligned), as written by dsattn_quantize_mxfp8: element x of block b of a row
  * stands for e4m3(x) * 2^(scale[b] - 127).  S = Q K^T is computed from these values with
  * fp32 accumulation; v stays bf16, and the rule, the softmax and P V are as in the bf16
- * path.  Supported for the dense, BLASST and DynSparse rules with tile_q = 128 and
- * ascending key order (DSATTN_EUNSUPPORTED otherwise), not by the reordered entry point.
+ * path.  Supported for the dense, BLASST and DynSparse rules at both decision units
+ * (tile_q = 128 or 32) and both key orders; not for mask reuse or by the reordered entry
+ * point (DSATTN_EUNSUPPORTED).
  */
 
 /*

@@ -271,11 +271,11 @@ def dsattn_attn_fwd_ex(rule, param, q, k, v, o=None, scale=None, tile_q=TILE_Q,
 
 
 def dsattn_attn_fwd_mxfp8(rule, param, q8, q_scales, k8, k_scales, v, o=None, scale=None,
-                          stats_out=None, mask_out=None, lse_out=None, stream=None):
+                          tile_q=TILE_Q, stats_out=None, mask_out=None, lse_out=None,
+                          stream=None, key_order=ORDER_ASCENDING):
     """A rule with MX-FP8 Q and K (``dsattn_qk_format`` DSATTN_QK_MXFP8): q8 / k8 are uint8
     E4M3 codes [B, H, N, 128] and q_scales / k_scales their uint8 E8M0 exponents
-    [B, H, N, 4], as returned by ``dsattn_quantize_mxfp8``; v is bf16.  tile_q is 128 and
-    the key order ascending."""
+    [B, H, N, 4], as returned by ``dsattn_quantize_mxfp8``; v is bf16."""
     import torch
 
     o = torch.empty_like(v) if o is None else o
@@ -287,10 +287,10 @@ def dsattn_attn_fwd_mxfp8(rule, param, q8, q_scales, k8, k_scales, v, o=None, sc
         if not t.is_cuda or not t.is_contiguous() or tuple(t.shape) != (B, H, N, n):
             raise ValueError(f"{name} must be a contiguous GPU tensor of shape {(B, H, N, n)}")
     scale = 1.0 / math.sqrt(d) if scale is None else scale
-    st, mk, ls = _buffers(B, H, N, stats_out, mask_out, lse_out, TILE_Q)
+    st, mk, ls = _buffers(B, H, N, stats_out, mask_out, lse_out, tile_q)
     a = DsAttnArgs(rule, param, q8.data_ptr(), k8.data_ptr(), v.data_ptr(), o.data_ptr(),
-                   B, H, N, d, scale, TILE_Q, TILE_K, _stream(stream), st, mk, ls,
-                   ORDER_ASCENDING, None, QK_MXFP8, q_scales.data_ptr(), k_scales.data_ptr())
+                   B, H, N, d, scale, tile_q, TILE_K, _stream(stream), st, mk, ls,
+                   key_order, None, QK_MXFP8, q_scales.data_ptr(), k_scales.data_ptr())
     _check(lib().dsattn_attn_fwd_ex(ctypes.byref(a)), "dsattn_attn_fwd_ex")
     return o
 

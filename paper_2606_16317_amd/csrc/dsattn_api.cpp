@@ -75,14 +75,8 @@ int check_problem(const dsattn_args& a) {
     return fail(DSATTN_EINVAL, "unknown key order %d", a.key_order);
   if (a.qk_format != DSATTN_QK_BF16 && a.qk_format != DSATTN_QK_MXFP8)
     return fail(DSATTN_EINVAL, "unknown qk format %d", a.qk_format);
-  if (a.qk_format == DSATTN_QK_MXFP8) {
-    if (a.rule == DSATTN_RULE_MASK)
-      return fail(DSATTN_EUNSUPPORTED, "mask reuse takes bf16 q and k");
-    if (a.tile_q != kTileQ)
-      return fail(DSATTN_EUNSUPPORTED, "MX-FP8 q and k need tile_q = 128");
-    if (a.key_order != DSATTN_ORDER_ASCENDING)
-      return fail(DSATTN_EUNSUPPORTED, "MX-FP8 q and k need the ascending key order");
-  }
+  if (a.qk_format == DSATTN_QK_MXFP8 && a.rule == DSATTN_RULE_MASK)
+    return fail(DSATTN_EUNSUPPORTED, "mask reuse takes bf16 q and k");
   if (a.rule == DSATTN_RULE_MASK) {
     if (a.key_order != DSATTN_ORDER_ASCENDING)
       return fail(DSATTN_EUNSUPPORTED, "mask reuse visits key tiles in ascending order only");

@@ -1059,14 +1059,14 @@ hipError_t launch_unit(int rule, const FwdParams& p, dim3 grid, hipStream_t stre
   return hipGetLastError();
 }
 
-template <int UNIT>
+template <int UNIT, bool Q8>
 hipError_t launch_order(int rule, const FwdParams& p, dim3 grid, hipStream_t stream) {
   if (p.key_order == kOrderDiagonal && rule != kRuleDense) {
     const int chunk = (p.n_qt + kXcds - 1) / kXcds;
-    return launch_unit<UNIT, kOrderDiagonal>(rule, p, dim3((unsigned)(chunk * kXcds), grid.y),
-                                             stream);
+    return launch_unit<UNIT, kOrderDiagonal, Q8>(rule, p,
+                                                 dim3((unsigned)(chunk * kXcds), grid.y), stream);
   }
-  return launch_unit<UNIT, kOrderAscending>(rule, p, grid, stream);
+  return launch_unit<UNIT, kOrderAscending, Q8>(rule, p, grid, stream);
 }
 
 }  // namespace
@@ -1085,14 +1085,14 @@ hipError_t launch_fa_fwd(int rule, int unit_rows, const FwdParams& p, int bh,
     return hipGetLastError();
   }
   if (p.qk_format == kQkMxfp8) {
-    // MX-FP8 Q K^T: 128-row decision units, ascending key order.
-    if (unit_rows != kTQ || p.key_order != kOrderAscending || p.q8 == nullptr ||
-        p.k8 == nullptr || p.q_scales == nullptr || p.k_scales == nullptr)
+    if (p.q8 == nullptr || p.k8 == nullptr || p.q_scales == nullptr || p.k_scales == nullptr)
       return hipErrorInvalidValue;
-    return launch_unit<kTQ, kOrderAscending, true>(rule, p, grid, stream);
+    if (unit_rows == kTQ) return launch_order<kTQ, true>(rule, p, grid, stream);
+    if (unit_rows == 32) return launch_order<32, true>(rule, p, grid, stream);
+    return hipErrorInvalidValue;
   }
-  if (unit_rows == kTQ) return launch_order<kTQ>(rule, p, grid, stream);
-  if (unit_rows == 32) return launch_order<32>(rule, p, grid, stream);
+  if (unit_rows == kTQ) return launch_order<kTQ, false>(rule, p, grid, stream);
+  if (unit_rows == 32) return launch_order<32, false>(rule, p, grid, stream);
   return hipErrorInvalidValue;
 }
 

@@ -98,13 +98,13 @@ class Report:
 
 
 def compare(q, k, v, g: GpuRun, rule: str, param: float, scale: float, tiles=None,
-            tile_q: int = TILE_Q) -> Report:
+            tile_q: int = TILE_Q, key_order: str = "ascending") -> Report:
     """Teacher-forced comparison of a GPU run with the oracle over ``tiles`` (b, h, qi),
     where qi counts query tiles of ``tile_q`` rows (the decision unit)."""
     B, H, N, d = q.shape
     name, thr = oracle_rule(rule, param, N)
     run = oracle.rule_attention(q, k, v, scale, name, thr, tile_q, TILE_K, tiles=tiles,
-                                forced_mask=g.mask)
+                                forced_mask=g.mask, key_order=key_order)
     mism, worst = 0, 0.0
     num = den = dnum = 0.0
     max_abs = lse_err = 0.0

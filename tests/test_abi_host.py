@@ -297,10 +297,10 @@ def test_qk_format_argument_checks():
         return L.dsattn_attn_fwd_ex(ctypes.byref(a)), pkg.last_error()
 
     assert call(qk_format=7) == (-1, "unknown qk format 7")
-    rc, err = call(tile_q=32)
-    assert rc == -2 and "tile_q = 128" in err
-    rc, err = call(key_order=pkg.ORDER_DIAGONAL)
-    assert rc == -2 and "ascending" in err
+    rc, err = call(tile_q=64)
+    assert rc == -2 and "tile shape" in err
+    rc, err = call(tile_q=32, key_order=pkg.ORDER_DIAGONAL)
+    assert rc == -1 and "non-null" in err           # supported: fails only on the pointers
     rc, err = call(rule=pkg.RULE_MASK)
     assert rc == -2 and "bf16" in err
     rc, err = call()

@@ -124,20 +124,21 @@ def quantised(q, k):
     return (qc, qs, kc, ks), (dequantize_mxfp8(qc, qs), dequantize_mxfp8(kc, ks))
 
 
-def run_gpu_q8(qc, qs, kc, ks, vd, rule, param, scale=SCALE):
+def run_gpu_q8(qc, qs, kc, ks, vd, rule, param, scale=SCALE, tile_q=128, key_order=0):
     import torch
     import paper_2606_16317_amd as dsa
 
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
     B, H, N, d = vd.shape
-    n_qt, n_kt = -(-N // 128), -(-N // 64)
+    n_qt, n_kt = -(-N // tile_q), -(-N // 64)
     o = torch.empty_like(vd)
     stats = torch.full((B * H * 4,), -7, dtype=torch.int64, device=vd.device)
     mask = torch.full((B * H * n_qt * n_kt,), 7, dtype=torch.uint8, device=vd.device)
     lse = torch.full((B * H * N,), float("nan"), dtype=torch.float32, device=vd.device)
     args = [dev(a) if isinstance(a, np.ndarray) else a for a in (qc, qs, kc, ks)]
     dsa.dsattn_attn_fwd_mxfp8(RULE_NAMES[rule], param, *args, vd, o, scale=scale,
-                              stats_out=stats, mask_out=mask, lse_out=lse)
+                              tile_q=tile_q, stats_out=stats, mask_out=mask, lse_out=lse,
+                              key_order=key_order)
     torch.cuda.synchronize()
     return GpuRun(from_device_bf16(o), mask.cpu().numpy().reshape(B, H, n_qt, n_kt),
                   lse.cpu().numpy().reshape(B, H, N), stats.cpu().numpy().reshape(B, H, 4))
@@ -183,6 +184,41 @@ def test_q8_attention_concentrated_heads_skip(peaked_q8, rule, param):
     assert_parity(rep)
     assert rep.sparsity > 0.1
     assert (g.stats == expected_stats_from_mask(g.mask, q.shape[2])).all()
+
+
+@pytest.mark.parametrize("tile_q,order", [(32, "ascending"), (128, "diagonal"),
+                                           (32, "diagonal")])
+@pytest.mark.parametrize("rule,param", [("dynsparse_lambda", -6.0), ("dynsparse_recall", 0.9),
+                                        ("blasst", 1e-2), ("dense", 0.0)])
+def test_q8_attention_decision_units_and_orders(peaked_q8, tile_q, order, rule, param):
+    """The quantised path at 32-row decision units and in diagonal-first key order: the
+    oracle runs the same unit and order on the dequantised inputs."""
+    (q, k, v), codes, (qf, kf), vd = peaked_q8
+    announce(f"q8 peaked tile_q={tile_q} order={order} rule={rule} param={param}")
+    g = run_gpu_q8(*codes, vd, rule, param, tile_q=tile_q,
+                   key_order=1 if order == "diagonal" else 0)
+    N = q.shape[2]
+    rep = compare(qf, kf, v, g, rule, param, SCALE, tile_q=tile_q, key_order=order,
+                  tiles=sample_tiles(1, 4, N, per_head=5, seed=7, tile_q=tile_q))
+    print(rep, flush=True)
+    assert_parity(rep)
+    assert (g.stats == expected_stats_from_mask(g.mask, N, tile_q)).all()
+    if rule != "dense":
+        assert rep.sparsity > 0.1
+
+
+@pytest.mark.parametrize("N", [65, 1000])
+def test_q8_attention_ragged_units_and_orders(N):
+    q, k, v = make_random_qkv(2, 2, N, 128, 9100 + N, q_std=1.5, k_std=1.5)
+    codes, (qf, kf) = quantised(q, k)
+    vd = to_device(v)
+    for tile_q, order in ((32, 0), (128, 1), (32, 1)):
+        announce(f"q8 ragged N={N} tile_q={tile_q} order={order}")
+        g = run_gpu_q8(*codes, vd, "dynsparse_lambda", -3.0, tile_q=tile_q, key_order=order)
+        rep = compare(qf, kf, v, g, "dynsparse_lambda", -3.0, SCALE, tile_q=tile_q,
+                      key_order="diagonal" if order else "ascending")
+        assert_parity(rep)
+        assert (g.stats == expected_stats_from_mask(g.mask, N, tile_q)).all()
 
 
 def test_q8_attention_from_gpu_quantisation_is_identical():
