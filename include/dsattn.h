@@ -23,10 +23,13 @@
  * Conventions shared by every entry point
  * ---------------------------------------
  * Layout: q, k, v, o are contiguous bf16 arrays [B][H][N][d], row-major (d fastest).
- * Shapes: d must be 128; (tile_q, tile_k) must be (128, 64) or (32, 64).  tile_k is the
- *   key tile; tile_q is the number of query rows that share one skip decision ("query
- *   tile" below): 128 decides per workgroup tile, 32 lets every 32-row slice decide on
- *   its own (a finer granularity of the same rule, which the paper leaves open).  B, H,
+ * Shapes: d must be 128; tile_q is 128 or 32 and tile_k 64 or 128.  tile_k is the key
+ *   tile B_c, the number of keys one skip decision covers (Section 4.2.1 uses 128 for the
+ *   14B model; 128 is computed as two 64-key tiles deciding together and visits keys in
+ *   ascending order only); tile_q is the number of query rows that share one skip
+ *   decision ("query tile" below): 128 decides per workgroup tile, 32 lets every 32-row
+ *   slice decide on its own (a finer granularity of the same rule, which the paper
+ *   leaves open).  B, H,
  *   N >= 0 and B*H <= 65535; B == 0, H == 0 or N == 0 is an empty problem: nothing is
  *   read or written except stats_out, which is zeroed.
  * Memory: every pointer is a device pointer allocated by the caller on the current HIP

@@ -182,11 +182,11 @@ def _out(q, o):
     return torch.empty_like(q) if o is None else o
 
 
-def _buffers(B, H, N, stats_out, mask_out=None, lse_out=None, tile_q=TILE_Q):
+def _buffers(B, H, N, stats_out, mask_out=None, lse_out=None, tile_q=TILE_Q, tile_k=TILE_K):
     import torch
 
     n_qt = -(-N // max(1, tile_q))
-    n_kt = -(-N // TILE_K)
+    n_kt = -(-N // max(1, tile_k))
     return (_ptr(stats_out, B * H * 4, (torch.int64, torch.uint64), "stats_out"),
             _ptr(mask_out, B * H * n_qt * n_kt, (torch.uint8,), "mask_out"),
             _ptr(lse_out, B * H * N, (torch.float32,), "lse_out"))
@@ -258,7 +258,7 @@ def dsattn_attn_fwd_ex(rule, param, q, k, v, o=None, scale=None, tile_q=TILE_Q,
     o = _out(q, o)
     B, H, N, d = _shape(q, k, v, o)
     scale = 1.0 / math.sqrt(d) if scale is None else scale
-    st, mk, ls = _buffers(B, H, N, stats_out, mask_out, lse_out, tile_q)
+    st, mk, ls = _buffers(B, H, N, stats_out, mask_out, lse_out, tile_q, tile_k)
     mi = None
     if mask_in is not None:
         n_qu = -(-N // max(1, tile_q))
@@ -272,7 +272,7 @@ def dsattn_attn_fwd_ex(rule, param, q, k, v, o=None, scale=None, tile_q=TILE_Q,
 
 def dsattn_attn_fwd_mxfp8(rule, param, q8, q_scales, k8, k_scales, v, o=None, scale=None,
                           tile_q=TILE_Q, stats_out=None, mask_out=None, lse_out=None,
-                          stream=None, key_order=ORDER_ASCENDING):
+                          stream=None, key_order=ORDER_ASCENDING, tile_k=TILE_K):
     """A rule with MX-FP8 Q and K (``dsattn_qk_format`` DSATTN_QK_MXFP8): q8 / k8 are uint8
     E4M3 codes [B, H, N, 128] and q_scales / k_scales their uint8 E8M0 exponents
     [B, H, N, 4], as returned by ``dsattn_quantize_mxfp8``; v is bf16."""
@@ -287,9 +287,9 @@ def dsattn_attn_fwd_mxfp8(rule, param, q8, q_scales, k8, k_scales, v, o=None, sc
         if not t.is_cuda or not t.is_contiguous() or tuple(t.shape) != (B, H, N, n):
             raise ValueError(f"{name} must be a contiguous GPU tensor of shape {(B, H, N, n)}")
     scale = 1.0 / math.sqrt(d) if scale is None else scale
-    st, mk, ls = _buffers(B, H, N, stats_out, mask_out, lse_out, tile_q)
+    st, mk, ls = _buffers(B, H, N, stats_out, mask_out, lse_out, tile_q, tile_k)
     a = DsAttnArgs(rule, param, q8.data_ptr(), k8.data_ptr(), v.data_ptr(), o.data_ptr(),
-                   B, H, N, d, scale, tile_q, TILE_K, _stream(stream), st, mk, ls,
+                   B, H, N, d, scale, tile_q, tile_k, _stream(stream), st, mk, ls,
                    key_order, None, QK_MXFP8, q_scales.data_ptr(), k_scales.data_ptr())
     _check(lib().dsattn_attn_fwd_ex(ctypes.byref(a)), "dsattn_attn_fwd_ex")
     return o
@@ -407,7 +407,7 @@ def dsattn_attn_fwd_reordered(rule, param, q, k, v, q_index, kv_index, o=None, s
     o = _out(q, o)
     B, H, N, d = _shape(q, k, v, o)
     scale = 1.0 / math.sqrt(d) if scale is None else scale
-    st, mk, ls = _buffers(B, H, N, stats_out, mask_out, lse_out, tile_q)
+    st, mk, ls = _buffers(B, H, N, stats_out, mask_out, lse_out, tile_q, tile_k)
     for name, t in (("q_index", q_index), ("kv_index", kv_index)):
         if t.dtype != torch.int32 or not t.is_cuda or not t.is_contiguous() or t.numel() != N:
             raise ValueError(f"{name} must be a contiguous int32 GPU tensor of N={N} entries")

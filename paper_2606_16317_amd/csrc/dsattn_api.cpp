@@ -22,6 +22,7 @@ thread_local std::string g_last_error;
 constexpr int kHeadDim = 128;
 constexpr int kTileQ = 128;
 constexpr int kTileK = 64;
+constexpr int kTileKPair = 128;  // one decision per two 64-key tiles
 constexpr int kUnitWave = 32;  // tile_q = 32: each wave's 32 rows decide on their own
 constexpr int kMaxMaskTiles = 4096;  // key tiles per head the mask-reuse kernel can list
 constexpr double kLog2e = 1.4426950408889634074;
@@ -63,9 +64,10 @@ int check_problem(const dsattn_args& a) {
     return fail(DSATTN_EINVAL, "scale must be finite and > 0 (got %g)", (double)a.scale);
   if (a.d != kHeadDim)
     return fail(DSATTN_EUNSUPPORTED, "head dimension %d is not supported (only 128)", a.d);
-  if ((a.tile_q != kTileQ && a.tile_q != kUnitWave) || a.tile_k != kTileK)
+  if ((a.tile_q != kTileQ && a.tile_q != kUnitWave) ||
+      (a.tile_k != kTileK && a.tile_k != kTileKPair))
     return fail(DSATTN_EUNSUPPORTED,
-                "tile shape %d x %d is not supported (128 x 64, or 32 x 64 for per-wave decisions)",
+                "tile shape %d x %d is not supported (tile_q 128 or 32, tile_k 64 or 128)",
                 a.tile_q, a.tile_k);
   const long long bh = (long long)a.B * (long long)a.H;
   if (bh > 65535) return fail(DSATTN_EINVAL, "B*H must be <= 65535 (got %lld)", bh);
@@ -77,6 +79,12 @@ int check_problem(const dsattn_args& a) {
     return fail(DSATTN_EINVAL, "unknown qk format %d", a.qk_format);
   if (a.qk_format == DSATTN_QK_MXFP8 && a.rule == DSATTN_RULE_MASK)
     return fail(DSATTN_EUNSUPPORTED, "mask reuse takes bf16 q and k");
+  if (a.tile_k == kTileKPair) {
+    if (a.key_order != DSATTN_ORDER_ASCENDING)
+      return fail(DSATTN_EUNSUPPORTED, "tile_k = 128 visits key tiles in ascending order only");
+    if (a.rule == DSATTN_RULE_MASK)
+      return fail(DSATTN_EUNSUPPORTED, "mask reuse takes tile_k = 64");
+  }
   if (a.rule == DSATTN_RULE_MASK) {
     if (a.key_order != DSATTN_ORDER_ASCENDING)
       return fail(DSATTN_EUNSUPPORTED, "mask reuse visits key tiles in ascending order only");
@@ -160,6 +168,8 @@ int launch_attention(const dsattn_args& a, const Request& rq) {
   p.key_order = a.key_order == DSATTN_ORDER_DIAGONAL ? dsattn::kOrderDiagonal
                                                      : dsattn::kOrderAscending;
   p.mask_in = a.rule == DSATTN_RULE_MASK ? a.mask_in : nullptr;
+  p.key_tile = a.tile_k;
+  p.n_kd = (a.N + a.tile_k - 1) / a.tile_k;
   const bool q8 = a.qk_format == DSATTN_QK_MXFP8;
   p.qk_format = q8 ? dsattn::kQkMxfp8 : dsattn::kQkBf16;
   p.q8 = q8 ? static_cast<const uint8_t*>(a.q) : nullptr;

@@ -679,11 +679,136 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
   }
 }
 
+// ---- 128-key decisions -------------------------------------------------------------
+// With B_c = 128 one decision covers two consecutive 64-key tiles 2m, 2m+1 (a "pair"),
+// visited in ascending order.  The pipeline keeps its 64-key steps and two score tiles in
+// registers:
+//   * first step of pair m (tile j = 2m, S_j already in registers): compute S_{j+1}, take
+//     the pair's row max over both, vote (Eq. 5 against the LSE after pair m-1) and meet
+//     the other waves at a barrier in the middle of the step; if the pair is kept, form
+//     P_j and accumulate P_j V_j, the softmax running under the P.V MFMAs;
+//   * second step (tile j+1): the ordinary kept or skipped tile body, which also computes
+//     S of the next pair's first tile; no vote.
+// V tiles follow the same policy as with 64-key decisions: the next tile's V is
+// requested when the current pair is kept, and a kept pair after a skipped one fetches its
+// first V tile late.
+
+// Softmax of S_j (lazy reference max already updated) and O += P_j V_j: the first eight
+// elements up front, then two under each of the first twelve P.V MFMAs, so that P block s
+// is complete before MFMA 4 s reads it.
+__device__ __forceinline__ void softmax_pv_tile(RowState& rs, f32x16 (&o)[4],
+                                                const f32x16 (&s_cur)[2], float c,
+                                                const uint16_t* vt, int lane) {
+  const float neg_m = -rs.m_ref;
+  float psum = 0.f;
+  bf16x8 pf[4];
+  bf16x8 va[3];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) softmax_elem(s_cur, e, c, neg_m, psum, pf);
+  va[0] = v_operand(vt, 0, lane);
+  va[1] = v_operand(vt, 1, lane);
+  sched_fence();
+  __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    if (i + 2 < 16) va[(i + 2) % 3] = v_operand(vt, i + 2, lane);
+    o[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i % 3], pf[i >> 2], o[i & 3], 0, 0, 0);
+    if (i < 12) {
+      softmax_elem(s_cur, 8 + 2 * i, c, neg_m, psum, pf);
+      softmax_elem(s_cur, 9 + 2 * i, c, neg_m, psum, pf);
+    }
+    sched_fence();
+  }
+  __builtin_amdgcn_s_setprio(0);
+  rs.l_half += psum;
+}
+
+// First step of pair m = j / 2.  On entry s_cur holds S_j and mhat its row max; v_ready
+// tells whether V_j was requested in the previous step.  On exit s_next holds S_{j+1},
+// mhat the pair's row max, keep_own / keep_any the pair's decisions.
+template <int RULE, int UNIT, bool Q8>
+__device__ __forceinline__ void pair_first_step(int j, const f32x16 (&s_cur)[2],
+                                                f32x16 (&s_next)[2], float& mhat,
+                                                bool& keep_own, bool& keep_any, bool& v_ready,
+                                                RowState& rs, f32x16 (&o)[4],
+                                                const typename QFragOf<Q8>::type& qf,
+                                                Smem& sm, const LoopCtx& cx, SkipCount& sk) {
+  const int nb = (j + 1) & 1;
+  load_k_tile<Q8>(sm, j & 1, cx, (j + 2) * kTK);
+  if constexpr (Q8)
+    skipped_tile_q8(s_next, reinterpret_cast<const uint8_t*>(sm.k[nb]), sm.ks[nb], qf, cx.r,
+                    cx.g);
+  else
+    skipped_tile(s_next, sm.k[nb], qf, cx.r, cx.g);
+  // Keys past the end (a partial last tile, or no second tile at all) do not count.
+  if ((j + 2) * kTK > cx.N) mask_tail(s_next, (j + 1) * kTK, cx.N, cx.g);
+  const float mhat_pair = fmaxf(mhat, row_max(s_next) * cx.c);
+  if constexpr (RULE != kRuleDense) {
+    const bool wave_keeps = __ballot(cx.valid & row_keeps<RULE>(rs, mhat_pair, cx.thr)) != 0;
+    if (cx.lane == 0) sm.vote[0][cx.w] = wave_keeps ? 1 : 0;
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    keep_any = __builtin_amdgcn_readfirstlane(*reinterpret_cast<const uint32_t*>(sm.vote[0])) != 0;
+    keep_own = UNIT == kTQ ? keep_any : wave_keeps;
+  }
+  if (cx.mask_row != nullptr && (UNIT == kTQ ? cx.w == 0 : true) && cx.lane == 0)
+    cx.mask_row[j >> 1] = keep_own ? 0 : 1;
+  if (keep_any && !v_ready) {
+    load_tile_lds(sm.v[j & 1], cx.vrs, cx.voff, j * kTK, cx.w);
+    asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+  }
+  if (keep_any) load_tile_lds(sm.v[nb], cx.vrs, cx.voff, (j + 1) * kTK, cx.w);
+  if (keep_own) {
+    rescale_if_needed(rs, o, mhat_pair);
+    softmax_pv_tile(rs, o, s_cur, cx.c, sm.v[j & 1], cx.lane);
+  } else {
+    sk.tiles += 1;
+    sk.elems += (uint64_t)cx.rows_valid * (uint64_t)min(2 * kTK, cx.N - j * kTK);
+  }
+  v_ready = keep_any;
+  mhat = mhat_pair;
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Second step of the pair (tile j = 2m + 1, decisions from the first step): the tile
+// body, which also computes S_{j+1} of the next pair's first tile.
+template <int RULE, int UNIT, bool Q8>
+__device__ __forceinline__ void pair_second_step(int j, const f32x16 (&s_cur)[2],
+                                                 f32x16 (&s_next)[2], float& mhat,
+                                                 bool keep_own, bool keep_any, bool& v_ready,
+                                                 RowState& rs, f32x16 (&o)[4],
+                                                 const typename QFragOf<Q8>::type& qf,
+                                                 Smem& sm, const LoopCtx& cx) {
+  const int nb = (j + 1) & 1;
+  load_k_tile<Q8>(sm, j & 1, cx, (j + 2) * kTK);
+  if (keep_any) load_tile_lds(sm.v[nb], cx.vrs, cx.voff, (j + 1) * kTK, cx.w);
+  if (keep_own) {
+    if constexpr (Q8)
+      kept_tile_q8(rs, o, s_cur, mhat, cx.c, s_next, reinterpret_cast<const uint8_t*>(sm.k[nb]),
+                   sm.ks[nb], sm.v[j & 1], qf, cx.r, cx.g, cx.lane);
+    else
+      kept_tile(rs, o, s_cur, mhat, cx.c, s_next, sm.k[nb], sm.v[j & 1], qf, cx.r, cx.g,
+                cx.lane);
+  } else {
+    if constexpr (Q8)
+      skipped_tile_q8(s_next, reinterpret_cast<const uint8_t*>(sm.k[nb]), sm.ks[nb], qf, cx.r,
+                      cx.g);
+    else
+      skipped_tile(s_next, sm.k[nb], qf, cx.r, cx.g);
+  }
+  v_ready = keep_any;
+  if (j + 1 < cx.n_kt) {
+    if ((j + 2) * kTK > cx.N) mask_tail(s_next, (j + 1) * kTK, cx.N, cx.g);
+    mhat = row_max(s_next) * cx.c;
+  }
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 // UNIT: query rows per skip decision, 128 (the workgroup's tile) or 32 (one wave).
 // ORDER: key-tile visit order (ascending or diagonal-first).
 // Q8: Q and K in MX-FP8 (codes p.q8 / p.k8, exponents p.q_scales / p.k_scales), S = Q K^T
 // on the scaled fp8 MFMA; everything after S is the same as with bf16 Q and K.
-template <int RULE, int UNIT, int ORDER, bool Q8>
+// PAIR: one decision per 128 keys (two 64-key tiles), ascending order only.
+template <int RULE, int UNIT, int ORDER, bool Q8, bool PAIR = false>
 __global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads),
                           amdgpu_waves_per_eu(2, 2))) void
 fa_fwd_kernel(FwdParams p) {
@@ -739,7 +864,7 @@ fa_fwd_kernel(FwdParams p) {
   const int unit_row0 = unit * UNIT;
   cx.rows_valid = max(0, min(UNIT, N - unit_row0));
   cx.mask_row = (p.mask != nullptr && cx.rows_valid > 0)
-                    ? p.mask + ((size_t)bh * p.n_qu + unit) * p.n_kt
+                    ? p.mask + ((size_t)bh * p.n_qu + unit) * (PAIR ? p.n_kd : p.n_kt)
                     : nullptr;
   cx.diag_c = q0 / kTK;                               // < n_kt since q0 < N
   cx.diag_m = min(cx.diag_c, cx.n_kt - 1 - cx.diag_c);
@@ -802,13 +927,24 @@ fa_fwd_kernel(FwdParams p) {
   SkipCount sk;
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");  // K_0 consumed
 
-  // Unrolled by two so that S_j / S_{j+1} alternate between sa and sb without copies.
-  for (int j = 0; j < cx.n_kt; j += 2) {
-    key_tile_step<RULE, UNIT, ORDER, Q8>(j, sa, sb, mhat, keep_own, keep_any, vote, v_ready, rs,
-                                         o, qf, sm, cx, sk);
-    if (j + 1 < cx.n_kt)
-      key_tile_step<RULE, UNIT, ORDER, Q8>(j + 1, sb, sa, mhat, keep_own, keep_any, vote,
-                                           v_ready, rs, o, qf, sm, cx, sk);
+  if constexpr (PAIR) {
+    static_assert(ORDER == kOrderAscending, "128-key decisions walk keys in ascending order");
+    for (int j = 0; j < cx.n_kt; j += 2) {
+      pair_first_step<RULE, UNIT, Q8>(j, sa, sb, mhat, keep_own, keep_any, v_ready, rs, o, qf,
+                                      sm, cx, sk);
+      if (j + 1 < cx.n_kt)
+        pair_second_step<RULE, UNIT, Q8>(j + 1, sb, sa, mhat, keep_own, keep_any, v_ready, rs,
+                                         o, qf, sm, cx);
+    }
+  } else {
+    // Unrolled by two so that S_j / S_{j+1} alternate between sa and sb without copies.
+    for (int j = 0; j < cx.n_kt; j += 2) {
+      key_tile_step<RULE, UNIT, ORDER, Q8>(j, sa, sb, mhat, keep_own, keep_any, vote, v_ready,
+                                           rs, o, qf, sm, cx, sk);
+      if (j + 1 < cx.n_kt)
+        key_tile_step<RULE, UNIT, ORDER, Q8>(j + 1, sb, sa, mhat, keep_own, keep_any, vote,
+                                             v_ready, rs, o, qf, sm, cx, sk);
+    }
   }
 
   store_rows(p, o, rs, cx, head_off, bh, qrow);
@@ -816,7 +952,7 @@ fa_fwd_kernel(FwdParams p) {
   if (p.stats != nullptr && (UNIT == kTQ ? cx.w == 0 : true) && cx.lane == 0 &&
       cx.rows_valid > 0) {
     unsigned long long* st = reinterpret_cast<unsigned long long*>(p.stats) + (size_t)bh * 4;
-    atomicAdd(st + 0, (unsigned long long)cx.n_kt);
+    atomicAdd(st + 0, (unsigned long long)(PAIR ? p.n_kd : cx.n_kt));
     atomicAdd(st + 1, (unsigned long long)sk.tiles);
     atomicAdd(st + 2, (unsigned long long)cx.rows_valid * (unsigned long long)N);
     atomicAdd(st + 3, (unsigned long long)sk.elems);
@@ -1060,7 +1196,33 @@ hipError_t launch_unit(int rule, const FwdParams& p, dim3 grid, hipStream_t stre
 }
 
 template <int UNIT, bool Q8>
+hipError_t launch_pair(int rule, const FwdParams& p, dim3 grid, hipStream_t stream) {
+  const dim3 block(kThreads);
+  switch (rule) {
+    case kRuleDense:
+      hipLaunchKernelGGL((fa_fwd_kernel<kRuleDense, UNIT, kOrderAscending, Q8, true>), grid,
+                         block, 0, stream, p);
+      break;
+    case kRuleBlasst:
+      hipLaunchKernelGGL((fa_fwd_kernel<kRuleBlasst, UNIT, kOrderAscending, Q8, true>), grid,
+                         block, 0, stream, p);
+      break;
+    case kRuleDynSparse:
+      hipLaunchKernelGGL((fa_fwd_kernel<kRuleDynSparse, UNIT, kOrderAscending, Q8, true>), grid,
+                         block, 0, stream, p);
+      break;
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <int UNIT, bool Q8>
 hipError_t launch_order(int rule, const FwdParams& p, dim3 grid, hipStream_t stream) {
+  if (p.key_tile == 2 * kTK) {
+    if (p.key_order != kOrderAscending) return hipErrorInvalidValue;
+    return launch_pair<UNIT, Q8>(rule, p, grid, stream);
+  }
   if (p.key_order == kOrderDiagonal && rule != kRuleDense) {
     const int chunk = (p.n_qt + kXcds - 1) / kXcds;
     return launch_unit<UNIT, kOrderDiagonal, Q8>(rule, p,

@@ -32,6 +32,8 @@ struct FwdParams {
   const uint8_t* k8;
   const uint8_t* q_scales; // kQkMxfp8: E8M0 exponents [BH][N][4]
   const uint8_t* k_scales;
+  int key_tile;            // keys per skip decision: 64, or 128 (two 64-key tiles)
+  int n_kd;                // ceil(N / key_tile): decisions per row of the mask
 };
 
 // Enqueue one forward pass over `bh` heads on `stream`; unit_rows (128 or 32) is the

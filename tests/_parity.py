@@ -41,18 +41,19 @@ class GpuRun:
     stats: np.ndarray    # int64 [B,H,4]
 
 
-def run_gpu(qd, kd, vd, rule: str, param: float, scale: float, tile_q: int = TILE_Q) -> GpuRun:
+def run_gpu(qd, kd, vd, rule: str, param: float, scale: float, tile_q: int = TILE_Q,
+            tile_k: int = TILE_K) -> GpuRun:
     import torch
     import paper_2606_16317_amd as dsa
 
     B, H, N, d = qd.shape
-    n_qt, n_kt = -(-N // tile_q), -(-N // TILE_K)
+    n_qt, n_kt = -(-N // tile_q), -(-N // tile_k)
     o = torch.empty_like(qd)
     stats = torch.full((B * H * 4,), -7, dtype=torch.int64, device=qd.device)
     mask = torch.full((B * H * n_qt * n_kt,), 7, dtype=torch.uint8, device=qd.device)
     lse = torch.full((B * H * N,), float("nan"), dtype=torch.float32, device=qd.device)
     dsa.dsattn_attn_fwd_ex(RULE_NAMES[rule], param, qd, kd, vd, o, scale=scale, tile_q=tile_q,
-                           stats_out=stats, mask_out=mask, lse_out=lse)
+                           tile_k=tile_k, stats_out=stats, mask_out=mask, lse_out=lse)
     torch.cuda.synchronize()
     return GpuRun(from_device_bf16(o), mask.cpu().numpy().reshape(B, H, n_qt, n_kt),
                   lse.cpu().numpy().reshape(B, H, N), stats.cpu().numpy().reshape(B, H, 4))
@@ -69,11 +70,12 @@ def oracle_rule(rule: str, param: float, N: int):
     return "dynsparse", param
 
 
-def expected_stats_from_mask(mask: np.ndarray, N: int, tile_q: int = TILE_Q) -> np.ndarray:
+def expected_stats_from_mask(mask: np.ndarray, N: int, tile_q: int = TILE_Q,
+                             tile_k: int = TILE_K) -> np.ndarray:
     """Counters implied by a full skip mask [B,H,n_qt,n_kt]."""
     B, H, n_qt, n_kt = mask.shape
     rows = np.array([min(N, (i + 1) * tile_q) - i * tile_q for i in range(n_qt)], dtype=np.int64)
-    cols = np.array([min(N, (j + 1) * TILE_K) - j * TILE_K for j in range(n_kt)], dtype=np.int64)
+    cols = np.array([min(N, (j + 1) * tile_k) - j * tile_k for j in range(n_kt)], dtype=np.int64)
     area = rows[:, None] * cols[None, :]
     m = mask.astype(bool)
     out = np.zeros((B, H, 4), dtype=np.int64)
@@ -98,12 +100,12 @@ class Report:
 
 
 def compare(q, k, v, g: GpuRun, rule: str, param: float, scale: float, tiles=None,
-            tile_q: int = TILE_Q, key_order: str = "ascending") -> Report:
+            tile_q: int = TILE_Q, key_order: str = "ascending", tile_k: int = TILE_K) -> Report:
     """Teacher-forced comparison of a GPU run with the oracle over ``tiles`` (b, h, qi),
     where qi counts query tiles of ``tile_q`` rows (the decision unit)."""
     B, H, N, d = q.shape
     name, thr = oracle_rule(rule, param, N)
-    run = oracle.rule_attention(q, k, v, scale, name, thr, tile_q, TILE_K, tiles=tiles,
+    run = oracle.rule_attention(q, k, v, scale, name, thr, tile_q, tile_k, tiles=tiles,
                                 forced_mask=g.mask, key_order=key_order)
     mism, worst = 0, 0.0
     num = den = dnum = 0.0

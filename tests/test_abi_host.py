@@ -105,7 +105,8 @@ def _fwd(name, param, B=1, H=1, N=128, d=128, scale=0.1, tq=128, tk=64, ptr=None
     ("dynsparse_attn_fwd", 0.95, {"tq": 64}, -2, "tile"),
     ("dynsparse_attn_fwd", 0.95, {"tq": 32, "tk": 32}, -2, "tile"),
     ("dynsparse_attn_fwd", 0.95, {"tq": 32}, -1, "non-null"),   # 32 x 64 passes the shape check
-    ("dynsparse_attn_fwd", 0.95, {"tk": 128}, -2, "tile"),
+    ("dynsparse_attn_fwd", 0.95, {"tk": 128}, -1, "non-null"),  # 128-key decisions pass
+    ("dynsparse_attn_fwd", 0.95, {"tk": 96}, -2, "tile"),
     ("dynsparse_attn_fwd", 0.95, {"N": -1}, -1, ">= 0"),
     ("dynsparse_attn_fwd", 0.95, {"B": -2}, -1, ">= 0"),
     ("dynsparse_attn_fwd", 0.95, {"scale": 0.0}, -1, "scale"),
@@ -337,3 +338,20 @@ def test_key_mean_and_shifted_quantize_host_checks():
     assert rc == -1 and "multiple of 32" in err
     rc, err = _call_raw("dsattn_quantize_mxfp8_shift", None, p, None, None, 0, 128, 4, None)
     assert rc == 0 and err == ""
+
+
+def test_key_tile_128_restrictions():
+    pkg = _lib()
+    L = pkg.lib()
+    a = pkg.DsAttnArgs(pkg.RULE_DYNSPARSE_LAMBDA, -6.0, None, None, None, None, 1, 1, 256,
+                       128, 0.1, 128, 128, None, None, None, None, pkg.ORDER_DIAGONAL, None, 0,
+                       None, None)
+    assert L.dsattn_attn_fwd_ex(ctypes.byref(a)) == -2
+    assert "ascending" in pkg.last_error()
+    a.key_order, a.rule = pkg.ORDER_ASCENDING, pkg.RULE_MASK
+    assert L.dsattn_attn_fwd_ex(ctypes.byref(a)) == -2
+    assert "tile_k = 64" in pkg.last_error()
+    a.rule = pkg.RULE_BLASST
+    a.param = 0.01
+    assert L.dsattn_attn_fwd_ex(ctypes.byref(a)) == -1
+    assert "non-null" in pkg.last_error()

@@ -1,0 +1,207 @@
+"""GPU parity of 128-key skip decisions (tile_k = 128, B_c = 128 of Section 4.2.1) against
+the oracle run with 128-key tiles (``rule_attention(..., tile_k=128)``), teacher-forced on
+the GPU's mask.
+
+The kernel decides for two 64-key tiles together: the vote takes the row max over both
+and the LSE after the previous pair.  Every check of the 64-key path applies: decisions
+(mismatches only within the 1e-3 margin), outputs and LSE within the same tolerances,
+stats implied by the mask, the recall bound of Section 3.1 from the GPU's own LSE, ragged
+sequences where the last pair is partial or has a single tile, both decision units, and
+MX-FP8 Q and K.
+"""
+
+import math
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle.mxfp8 import dequantize_mxfp8, quantize_mxfp8
+from synth import make_random_qkv, make_video_qkv, workload_inputs
+
+from _parity import (GpuRun, RULE_NAMES, assert_parity, compare, expected_stats_from_mask,
+                     from_device_bf16, run_gpu, sample_tiles, to_device)
+
+pytestmark = pytest.mark.gpu
+
+SCALE = 1.0 / math.sqrt(128)
+TK = 128
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2606_16317_amd as dsa
+
+    dsa.lib()
+    return torch
+
+
+def announce(msg):
+    print(f"\n[case] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+def upload(q, k, v):
+    return to_device(q), to_device(k), to_device(v)
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    q, k, v, _ = workload_inputs("tiny")
+    return (q, k, v), upload(q, k, v)
+
+
+RULES = [("dense", 0.0), ("dynsparse_recall", 0.95), ("dynsparse_lambda", -4.0),
+         ("dynsparse_lambda", -6.0), ("dynsparse_lambda", -8.0), ("blasst", 0.1),
+         ("blasst", 0.01)]
+
+
+@pytest.mark.parametrize("tile_q", [128, 32])
+@pytest.mark.parametrize("rule,param", RULES)
+def test_tiny_workload_all_tiles(tiny, tile_q, rule, param):
+    (q, k, v), dev = tiny
+    announce(f"tile_k=128 tiny tile_q={tile_q} rule={rule} param={param}")
+    g = run_gpu(*dev, rule, param, SCALE, tile_q=tile_q, tile_k=TK)
+    rep = compare(q, k, v, g, rule, param, SCALE, tile_q=tile_q, tile_k=TK)
+    print(rep, flush=True)
+    assert_parity(rep)
+    assert (g.stats == expected_stats_from_mask(g.mask, q.shape[2], tile_q, TK)).all()
+    assert (g.mask[..., 0] == 0).all()              # the first key tile is always kept
+
+
+RAGGED = [(1, 1, 1), (1, 1, 64), (1, 1, 65), (1, 1, 128), (1, 1, 129), (1, 1, 191),
+          (1, 1, 192), (1, 1, 193), (2, 3, 257), (1, 2, 1000), (1, 1, 2047)]
+
+
+@pytest.mark.parametrize("B,H,N", RAGGED)
+@pytest.mark.parametrize("rule,param", [("dense", 0.0), ("dynsparse_lambda", -3.0),
+                                        ("blasst", 0.05)])
+def test_ragged_shapes(B, H, N, rule, param):
+    q, k, v = make_random_qkv(B, H, N, 128, 5000 + 1000 * B + 10 * H + N, q_std=1.5,
+                              k_std=1.5)
+    announce(f"tile_k=128 ragged B={B} H={H} N={N} rule={rule} param={param}")
+    for tile_q in (128, 32):
+        g = run_gpu(*upload(q, k, v), rule, param, SCALE, tile_q=tile_q, tile_k=TK)
+        assert_parity(compare(q, k, v, g, rule, param, SCALE, tile_q=tile_q, tile_k=TK))
+        assert (g.stats == expected_stats_from_mask(g.mask, N, tile_q, TK)).all()
+        assert not np.isnan(g.lse).any()
+
+
+@pytest.fixture(scope="module")
+def peaked():
+    q, k, v, _ = make_video_qkv(1, 4, (2, 16, 32), 6.0, 6.0, True, 31)
+    return (q, k, v), upload(q, k, v)
+
+
+@pytest.mark.parametrize("tile_q", [128, 32])
+@pytest.mark.parametrize("rule,param", [("dynsparse_recall", 0.9), ("dynsparse_lambda", -6.0),
+                                        ("blasst", 1e-2)])
+def test_concentrated_heads_skip(peaked, tile_q, rule, param):
+    (q, k, v), dev = peaked
+    announce(f"tile_k=128 peaked tile_q={tile_q} rule={rule} param={param}")
+    g = run_gpu(*dev, rule, param, SCALE, tile_q=tile_q, tile_k=TK)
+    rep = compare(q, k, v, g, rule, param, SCALE, tile_q=tile_q, tile_k=TK)
+    print(rep, flush=True)
+    assert_parity(rep)
+    assert rep.sparsity > 0.1
+    N = q.shape[2]
+    assert (g.stats == expected_stats_from_mask(g.mask, N, tile_q, TK)).all()
+    if rule == "dynsparse_recall":
+        # recall bound of Section 3.1 on every row, from the GPU's own kept-set LSE
+        for h in range(q.shape[1]):
+            s = SCALE * (oracle.bf16_to_f64(q[0, h]) @ oracle.bf16_to_f64(k[0, h]).T)
+            mx = s.max(axis=1)
+            lse_all = mx + np.log(np.exp(s - mx[:, None]).sum(axis=1))
+            recall = np.exp(g.lse[0, h].astype(np.float64) - lse_all)
+            assert recall.min() >= param - 2e-3
+
+
+def test_infinite_threshold_equals_dense(peaked):
+    """At recall 1 (lambda = -inf) and tau = 0 the 128-key rule kernels keep everything and
+    reproduce the 128-key dense kernel bit for bit."""
+    (q, k, v), dev = peaked
+    announce("tile_k=128 infinite thresholds vs dense")
+    d = run_gpu(*dev, "dense", 0.0, SCALE, tile_k=TK)
+    for rule, param in (("dynsparse_recall", 1.0), ("blasst", 0.0)):
+        g = run_gpu(*dev, rule, param, SCALE, tile_k=TK)
+        np.testing.assert_array_equal(g.o, d.o)
+        np.testing.assert_array_equal(g.lse, d.lse)
+        assert not g.mask.any()
+
+
+def test_128_key_decisions_skip_less_than_64(peaked):
+    """A 128-key tile is skipped only when both of its halves would be below the threshold
+    against the same LSE, so at one lambda it skips no more keys than 64-key decisions do
+    on these heads (checked, not a theorem: the LSE the halves see differs)."""
+    (q, k, v), dev = peaked
+    announce("tile_k=128 vs 64 sparsity at lambda=-6")
+    g128 = run_gpu(*dev, "dynsparse_lambda", -6.0, SCALE, tile_k=TK)
+    g64 = run_gpu(*dev, "dynsparse_lambda", -6.0, SCALE)
+    sp = lambda g: g.stats[..., 3].sum() / g.stats[..., 2].sum()
+    assert 0.0 < sp(g128) <= sp(g64) + 0.02
+
+
+@pytest.mark.parametrize("rule,param", [("dynsparse_lambda", -6.0), ("blasst", 1e-2),
+                                        ("dense", 0.0)])
+def test_mxfp8_with_128_key_decisions(peaked, rule, param):
+    import torch
+    import paper_2606_16317_amd as dsa
+
+    (q, k, v), dev = peaked
+    announce(f"tile_k=128 mxfp8 rule={rule} param={param}")
+    qc, qs = quantize_mxfp8(oracle.bf16_to_f64(q))
+    kc, ks = quantize_mxfp8(oracle.bf16_to_f64(k))
+    up = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    B, H, N, d = q.shape
+    n_kd = -(-N // TK)
+    o = torch.empty_like(dev[2])
+    stats = torch.full((B * H * 4,), -7, dtype=torch.int64, device="cuda")
+    mask = torch.full((B * H * (N // 128) * n_kd,), 7, dtype=torch.uint8, device="cuda")
+    lse = torch.full((B * H * N,), float("nan"), dtype=torch.float32, device="cuda")
+    dsa.dsattn_attn_fwd_mxfp8(RULE_NAMES[rule], param, up(qc), up(qs), up(kc), up(ks), dev[2],
+                              o, scale=SCALE, tile_k=TK, stats_out=stats, mask_out=mask,
+                              lse_out=lse)
+    torch.cuda.synchronize()
+    g = GpuRun(from_device_bf16(o), mask.cpu().numpy().reshape(B, H, N // 128, n_kd),
+               lse.cpu().numpy().reshape(B, H, N), stats.cpu().numpy().reshape(B, H, 4))
+    rep = compare(dequantize_mxfp8(qc, qs), dequantize_mxfp8(kc, ks), v, g, rule, param, SCALE,
+                  tile_k=TK, tiles=sample_tiles(B, H, N, per_head=4, seed=2))
+    print(rep, flush=True)
+    assert_parity(rep)
+    assert (g.stats == expected_stats_from_mask(g.mask, N, 128, TK)).all()
+
+
+def test_reordered_entry_point_identity_maps(peaked):
+    """The reordered entry point with identity maps reproduces the plain 128-key call."""
+    import torch
+    import paper_2606_16317_amd as dsa
+
+    (q, k, v), (qd, kd, vd) = peaked
+    announce("tile_k=128 reordered identity")
+    N = q.shape[2]
+    idx = torch.arange(N, dtype=torch.int32, device="cuda")
+    a = dsa.dsattn_attn_fwd_ex(dsa.RULE_DYNSPARSE_LAMBDA, -6.0, qd, kd, vd, scale=SCALE,
+                               tile_k=TK)
+    b = dsa.dsattn_attn_fwd_reordered(dsa.RULE_DYNSPARSE_LAMBDA, -6.0, qd, kd, vd, idx, idx,
+                                      scale=SCALE, tile_k=TK)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+@pytest.mark.slow
+def test_wan720p_sampled_tiles():
+    q, k, v, _ = workload_inputs("wan720p")
+    announce("tile_k=128 wan720p sampled, lambda=-6 and recall 0.95")
+    dev = upload(q, k, v)
+    B, H, N, d = q.shape
+    tiles = sample_tiles(B, H, N, per_head=3, heads=[(0, 0), (0, 21)], seed=4)
+    for rule, param in (("dynsparse_lambda", -6.0), ("dynsparse_recall", 0.95)):
+        g = run_gpu(*dev, rule, param, SCALE, tile_k=TK)
+        rep = compare(q, k, v, g, rule, param, SCALE, tiles=tiles, tile_k=TK)
+        print(rep, flush=True)
+        assert_parity(rep)
+        assert (g.stats == expected_stats_from_mask(g.mask, N, 128, TK)).all()
