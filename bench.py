@@ -351,6 +351,7 @@ def sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop):
     B, H, N = w.B, w.H, w.N
     # 128-row decisions in ascending key order (the default); then every wave's 32 rows
     # deciding on their own (tile_q = 32); then the diagonal-first key order.
+    # 128-key decisions (tile_k = 128) close the list.
     asc, diag = dsa.ORDER_ASCENDING, dsa.ORDER_DIAGONAL
     points = [("dense", 0.0, TILE_Q, asc)] + \
              [("dynsparse_recall", r, TILE_Q, asc) for r in (0.90, 0.95, 0.98, 0.99)] + \
@@ -362,23 +363,31 @@ def sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop):
              [("dynsparse_recall", 0.95, TILE_Q, diag), ("dynsparse_lambda", -6.0, TILE_Q, diag),
               ("dynsparse_lambda", -8.0, TILE_Q, diag), ("dynsparse_lambda", -10.0, TILE_Q, diag),
               ("blasst", 1e-2, TILE_Q, diag), ("dynsparse_lambda", -8.0, 32, diag)]
+    points = [pt + (TILE_K,) for pt in points] + \
+             [("dense", 0.0, TILE_Q, asc, 128), ("dynsparse_recall", 0.95, TILE_Q, asc, 128),
+              ("dynsparse_lambda", -6.0, TILE_Q, asc, 128),
+              ("dynsparse_lambda", -8.0, TILE_Q, asc, 128),
+              ("dynsparse_lambda", -10.0, TILE_Q, asc, 128), ("blasst", 1e-2, TILE_Q, asc, 128),
+              ("dynsparse_lambda", -6.0, 32, asc, 128)]
     rule_ids = {"dense": dsa.RULE_DENSE, "dynsparse_recall": dsa.RULE_DYNSPARSE_RECALL,
                 "dynsparse_lambda": dsa.RULE_DYNSPARSE_LAMBDA, "blasst": dsa.RULE_BLASST}
     dense_ms = None
-    for rule, p, tq, order in points:
-        out = od if rule == "dense" else o
+    for rule, p, tq, order, tk in points:
+        out = od if (rule == "dense" and tk == TILE_K) else o
         fn = lambda: dsa.dsattn_attn_fwd_ex(rule_ids[rule], p, qd, kd, vd, out, scale=scale,
-                                            tile_q=tq, stats_out=stats, key_order=order)
-        print(f"[sweep] {rule} {p} tile_q={tq} order={order}", file=sys.stderr, flush=True)
+                                            tile_q=tq, tile_k=tk, stats_out=stats,
+                                            key_order=order)
+        print(f"[sweep] {rule} {p} tile_q={tq} tile_k={tk} order={order}", file=sys.stderr,
+              flush=True)
         ms = time_calls(fn, args.steps, args.warmup)
         st = stats.cpu().numpy().reshape(B * H, 4)
-        if rule == "dense":
+        if rule == "dense" and tk == TILE_K:
             dense_ms = ms
             rel = 0.0
         else:
             rel = float((o.float() - od.float()).pow(2).sum().sqrt() /
                         od.float().pow(2).sum().sqrt())
-        rec = {"workload": w.name, "rule": rule, "param": p, "tile_q": tq,
+        rec = {"workload": w.name, "rule": rule, "param": p, "tile_q": tq, "tile_k": tk,
                "key_order": "diagonal" if order == diag else "ascending", "ms": ms,
                "effective_tflops": dense_flop / (ms * 1e-3) / 1e12,
                "actual_tflops": algorithmic_flops(st) / (ms * 1e-3) / 1e12,
