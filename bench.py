@@ -203,7 +203,7 @@ def traffic_summary(fetch_dir, write_dir, workload, command):
                 continue
             kib = float(r["Counter_Value"])
             # DynSparse rule, 128-row units, ascending order, bf16 Q and K
-            if re.search(r"fa_fwd_kernel<2, 128, 0, false>", r["Kernel_Name"]):
+            if re.search(r"fa_fwd_kernel<2, 128, 0, false(, 64)?>", r["Kernel_Name"]):
                 vals["main"].append(kib)
             elif "AUnaryFunctor" in r["Kernel_Name"] or "MulFunctor" in r["Kernel_Name"]:
                 vals["copy"].append(kib)

@@ -23,6 +23,7 @@ constexpr int kHeadDim = 128;
 constexpr int kTileQ = 128;
 constexpr int kTileK = 64;
 constexpr int kTileKPair = 128;  // one decision per two 64-key tiles
+constexpr int kTileKHalf = 32;   // two decisions per 64-key tile
 constexpr int kUnitWave = 32;  // tile_q = 32: each wave's 32 rows decide on their own
 constexpr int kMaxMaskTiles = 4096;  // key tiles per head the mask-reuse kernel can list
 constexpr double kLog2e = 1.4426950408889634074;
@@ -65,9 +66,9 @@ int check_problem(const dsattn_args& a) {
   if (a.d != kHeadDim)
     return fail(DSATTN_EUNSUPPORTED, "head dimension %d is not supported (only 128)", a.d);
   if ((a.tile_q != kTileQ && a.tile_q != kUnitWave) ||
-      (a.tile_k != kTileK && a.tile_k != kTileKPair))
+      (a.tile_k != kTileK && a.tile_k != kTileKPair && a.tile_k != kTileKHalf))
     return fail(DSATTN_EUNSUPPORTED,
-                "tile shape %d x %d is not supported (tile_q 128 or 32, tile_k 64 or 128)",
+                "tile shape %d x %d is not supported (tile_q 128 or 32, tile_k 32, 64 or 128)",
                 a.tile_q, a.tile_k);
   const long long bh = (long long)a.B * (long long)a.H;
   if (bh > 65535) return fail(DSATTN_EINVAL, "B*H must be <= 65535 (got %lld)", bh);
@@ -79,11 +80,14 @@ int check_problem(const dsattn_args& a) {
     return fail(DSATTN_EINVAL, "unknown qk format %d", a.qk_format);
   if (a.qk_format == DSATTN_QK_MXFP8 && a.rule == DSATTN_RULE_MASK)
     return fail(DSATTN_EUNSUPPORTED, "mask reuse takes bf16 q and k");
-  if (a.tile_k == kTileKPair) {
+  if (a.tile_k != kTileK) {
     if (a.key_order != DSATTN_ORDER_ASCENDING)
-      return fail(DSATTN_EUNSUPPORTED, "tile_k = 128 visits key tiles in ascending order only");
+      return fail(DSATTN_EUNSUPPORTED, "tile_k = %d visits key tiles in ascending order only",
+                  a.tile_k);
     if (a.rule == DSATTN_RULE_MASK)
       return fail(DSATTN_EUNSUPPORTED, "mask reuse takes tile_k = 64");
+    if (a.tile_k == kTileKHalf && a.qk_format != DSATTN_QK_BF16)
+      return fail(DSATTN_EUNSUPPORTED, "tile_k = 32 takes bf16 q and k");
   }
   if (a.rule == DSATTN_RULE_MASK) {
     if (a.key_order != DSATTN_ORDER_ASCENDING)

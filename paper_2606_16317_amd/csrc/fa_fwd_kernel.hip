@@ -70,6 +70,8 @@ struct Smem {
   alignas(16) uint16_t v[2][kTileElems];
   alignas(4) uint8_t vote[2][kWaves];        // one byte per wave, read back as one dword
   alignas(16) uint8_t ks[2][kTK * 4];        // MX-FP8 K: E8M0 exponents, 4 blocks per key
+  alignas(4) uint8_t vote_h1[2][kWaves];     // B_c = 32: second-half votes
+  alignas(4) uint8_t vote_mid[kWaves];       // B_c = 32: second-half votes taken mid-step
 };
 
 // Mask-reuse workgroups also hold the list of key tiles they visit (at most
@@ -803,16 +805,226 @@ __device__ __forceinline__ void pair_second_step(int j, const f32x16 (&s_cur)[2]
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// ---- 32-key decisions ---------------------------------------------------------------
+// With B_c = 32 every 64-key tile holds two decision tiles, its key halves h0 (S block 0)
+// and h1 (block 1), visited in ascending order.  h0 of tile j is voted at the end of step
+// j-1 against the LSE after tile j-1, as with 64-key decisions but on its own row max.
+// h1 is voted against the LSE after h0:
+//   * if h0 is skipped that LSE is the same, so h1 is voted together with h0;
+//   * if h0 is kept, the step computes the softmax of both halves under the MFMAs of
+//     S_{j+1} (h1 speculatively, its row sum kept apart), adds h0's sum, votes on h1 (an
+//     LDS exchange and a barrier for 128-row units, the wave alone for 32-row units) and
+//     then adds h1's sum and issues h1's eight P.V MFMAs only if h1 is kept.
+// The lazy reference max is raised to the larger half max of the tile whenever the tile
+// is entered with a kept half; a half skipped after that only lowers P of the other half
+// by a bounded factor (its max is below the LSE), never the LSE itself.
+
+// Raise the lazy reference max (as rescale_if_needed, without the BLASST running max).
+__device__ __forceinline__ void raise_reference(RowState& rs, f32x16 (&o)[4], float m_hat) {
+  const bool need = m_hat > rs.m_ref + kRescaleSlack;
+  if (__ballot(need) != 0) {
+    const float m_new = need ? m_hat : rs.m_ref;
+    const float alpha = exp2_fast(rs.m_ref - m_new);
+    rs.l_half *= alpha;
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
+    rs.m_ref = m_new;
+  }
+}
+
+// Row max of one 32-key block of S^T.
+__device__ __forceinline__ float block_max(const f32x16& st) {
+  float mx = st[0];
+#pragma unroll
+  for (int v = 1; v < 16; ++v) mx = fmaxf(mx, st[v]);
+  return half_max(mx);
+}
+
+// S_{j+1} = K_{j+1} Q^T with the softmax of both halves of S_j under its 16 MFMAs (block
+// b relative to reference -neg_m_b; -inf makes a block contribute nothing), the row sums
+// of the halves kept apart.  Also reads the first two V operands.
+__device__ __forceinline__ void qk_softmax_halves(const f32x16 (&s_cur)[2], float c,
+                                                  float neg_m0, float neg_m1, float& psum0,
+                                                  float& psum1, bf16x8 (&pf)[4],
+                                                  bf16x8 (&va)[3], f32x16 (&s_next)[2],
+                                                  const uint16_t* kt, const uint16_t* vt,
+                                                  const bf16x8 (&qf)[8], int r, int g,
+                                                  int lane) {
+  bf16x8 ka[3];
+  ka[0] = k_operand(kt, 0, r, g);
+  ka[1] = k_operand(kt, 1, r, g);
+  sched_fence();
+  __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    if (i + 2 < 16)
+      ka[(i + 2) % 3] = k_operand(kt, i + 2, r, g);
+    else
+      va[i - 14] = v_operand(vt, i - 14, lane);
+    f32x16& acc = s_next[i & 1];
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[i % 3], qf[i >> 1],
+                                                  i < 2 ? f32x16{} : acc, 0, 0, 0);
+    if (i < 8) {
+      softmax_elem(s_cur, 2 * i, c, neg_m0, psum0, pf);
+      softmax_elem(s_cur, 2 * i + 1, c, neg_m0, psum0, pf);
+    } else {
+      softmax_elem(s_cur, 2 * i, c, neg_m1, psum1, pf);
+      softmax_elem(s_cur, 2 * i + 1, c, neg_m1, psum1, pf);
+    }
+    sched_fence();
+  }
+  __builtin_amdgcn_s_setprio(0);
+}
+
+// O += P V_j over the kept halves: MFMAs 0-7 cover keys 0-31, 8-15 keys 32-63.  va holds
+// the operands of MFMAs 0 and 1 on entry.
+__device__ __forceinline__ void pv_halves(f32x16 (&o)[4], const bf16x8 (&pf)[4], bf16x8 (&va)[3],
+                                          const uint16_t* vt, int lane, bool pv0, bool pv1) {
+  __builtin_amdgcn_s_setprio(1);
+  if (pv0) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      va[(i + 2) % 3] = v_operand(vt, i + 2, lane);
+      o[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i % 3], pf[i >> 2], o[i & 3], 0, 0, 0);
+      sched_fence();
+    }
+  } else {
+    va[8 % 3] = v_operand(vt, 8, lane);
+    va[9 % 3] = v_operand(vt, 9, lane);
+  }
+  if (pv1) {
+#pragma unroll
+    for (int i = 8; i < 16; ++i) {
+      if (i + 2 < 16) va[(i + 2) % 3] = v_operand(vt, i + 2, lane);
+      o[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i % 3], pf[i >> 2], o[i & 3], 0, 0, 0);
+      sched_fence();
+    }
+  }
+  __builtin_amdgcn_s_setprio(0);
+}
+
+// One 64-key step j with 32-key decisions.  On entry s_cur holds S_j and mh its half row
+// maxima (log2 units); vote[0] / vote[1] are the workgroup's vote words for h0 and for h1
+// against the same LSE (used for h1 when h0 is skipped), own[0] / own[1] this wave's own
+// votes (the decisions of 32-row units).  On exit the same for tile j+1.
+template <int RULE, int UNIT>
+__device__ __forceinline__ void half_tile_step(int j, const f32x16 (&s_cur)[2],
+                                               f32x16 (&s_next)[2], float (&mh)[2],
+                                               uint32_t (&vote)[2], bool (&own)[2],
+                                               bool& v_ready, RowState& rs, f32x16 (&o)[4],
+                                               const bf16x8 (&qf)[8], Smem& sm,
+                                               const LoopCtx& cx, SkipCount& sk) {
+  const int nb = (j + 1) & 1;
+  const bool has_next = (j + 1) < cx.n_kt;
+  load_tile_lds(sm.k[j & 1], cx.krs, cx.koff, (j + 2) * kTK, cx.w);
+  bool keep0 = true, keep1_pre = true, need_v = true;
+  if constexpr (RULE != kRuleDense) {
+    const bool any0 = __builtin_amdgcn_readfirstlane(vote[0]) != 0;
+    const bool any1 = __builtin_amdgcn_readfirstlane(vote[1]) != 0;
+    need_v = any0 || any1;
+    // (readfirstlane keeps the 32-row units' own votes visibly wave-uniform, so the
+    // compiler branches on them instead of predicating both paths)
+    keep0 = UNIT == kTQ ? any0 : __builtin_amdgcn_readfirstlane((int)own[0]) != 0;
+    keep1_pre = UNIT == kTQ ? any1 : __builtin_amdgcn_readfirstlane((int)own[1]) != 0;
+  }
+  if (need_v && !v_ready) {
+    load_tile_lds(sm.v[j & 1], cx.vrs, cx.voff, j * kTK, cx.w);
+    asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+  }
+  if (need_v) load_tile_lds(sm.v[nb], cx.vrs, cx.voff, (j + 1) * kTK, cx.w);
+
+  const bool h1_exists = j * kTK + 32 < cx.N;
+  bool keep1 = false;
+  bf16x8 pf[4], va[3];
+  float psum0 = 0.f, psum1 = 0.f;
+  if (keep0 || keep1_pre) {
+    // h0 kept (h1 decided below), or h0 skipped and h1 kept: one body, h0's elements
+    // relative to -inf in the second case.
+    raise_reference(rs, o, keep0 ? fmaxf(mh[0], mh[1]) : mh[1]);
+    if (keep0) rs.m_true = fmaxf(rs.m_true, mh[0]);
+    qk_softmax_halves(s_cur, cx.c, keep0 ? -rs.m_ref : -__builtin_inff(), -rs.m_ref, psum0,
+                      psum1, pf, va, s_next, sm.k[nb], sm.v[j & 1], qf, cx.r, cx.g, cx.lane);
+    sched_fence();
+    keep1 = true;
+    if (keep0) {
+      rs.l_half += psum0;
+      if constexpr (RULE != kRuleDense) {
+        const bool own1 = __ballot(cx.valid & row_keeps<RULE>(rs, mh[1], cx.thr)) != 0;
+        if constexpr (UNIT == kTQ) {
+          if (cx.lane == 0) sm.vote_mid[cx.w] = own1 ? 1 : 0;
+          asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+          keep1 = __builtin_amdgcn_readfirstlane(
+                      *reinterpret_cast<const uint32_t*>(sm.vote_mid)) != 0;
+        } else {
+          keep1 = __builtin_amdgcn_readfirstlane((int)own1) != 0;
+        }
+      }
+    }
+    if (keep1) {
+      rs.l_half += psum1;
+      rs.m_true = fmaxf(rs.m_true, mh[1]);
+    }
+    sched_fence();
+    pv_halves(o, pf, va, sm.v[j & 1], cx.lane, keep0, keep1);
+  } else {
+    skipped_tile(s_next, sm.k[nb], qf, cx.r, cx.g);
+  }
+  keep1 = keep1 && h1_exists;
+  if (cx.mask_row != nullptr && (UNIT == kTQ ? cx.w == 0 : true) && cx.lane == 0) {
+    cx.mask_row[2 * j] = keep0 ? 0 : 1;
+    if (h1_exists) cx.mask_row[2 * j + 1] = keep1 ? 0 : 1;
+  }
+  if (!keep0) {
+    sk.tiles += 1;
+    sk.elems += (uint64_t)cx.rows_valid * (uint64_t)min(32, cx.N - j * kTK);
+  }
+  if (h1_exists && !keep1) {
+    sk.tiles += 1;
+    sk.elems += (uint64_t)cx.rows_valid * (uint64_t)min(32, cx.N - j * kTK - 32);
+  }
+  v_ready = need_v;
+
+  bool next_own0 = true, next_own1 = true;
+  if (has_next) {
+    if (cx.ragged && j + 1 == cx.n_kt - 1) mask_tail(s_next, (j + 1) * kTK, cx.N, cx.g);
+    mh[0] = block_max(s_next[0]) * cx.c;
+    mh[1] = block_max(s_next[1]) * cx.c;
+    if constexpr (RULE != kRuleDense) {
+      next_own0 = __ballot(cx.valid & row_keeps<RULE>(rs, mh[0], cx.thr)) != 0;
+      next_own1 = __ballot(cx.valid & row_keeps<RULE>(rs, mh[1], cx.thr)) != 0;
+      if (cx.lane == 0) {
+        sm.vote[nb][cx.w] = next_own0 ? 1 : 0;
+        sm.vote_h1[nb][cx.w] = next_own1 ? 1 : 0;
+      }
+    }
+  }
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  if (has_next) {
+    if constexpr (RULE != kRuleDense) {
+      vote[0] = *reinterpret_cast<const uint32_t*>(sm.vote[nb]);
+      vote[1] = *reinterpret_cast<const uint32_t*>(sm.vote_h1[nb]);
+      own[0] = next_own0;
+      own[1] = next_own1;
+    }
+  }
+}
+
 // UNIT: query rows per skip decision, 128 (the workgroup's tile) or 32 (one wave).
 // ORDER: key-tile visit order (ascending or diagonal-first).
 // Q8: Q and K in MX-FP8 (codes p.q8 / p.k8, exponents p.q_scales / p.k_scales), S = Q K^T
 // on the scaled fp8 MFMA; everything after S is the same as with bf16 Q and K.
-// PAIR: one decision per 128 keys (two 64-key tiles), ascending order only.
-template <int RULE, int UNIT, int ORDER, bool Q8, bool PAIR = false>
+// BC: keys per skip decision: 64 (one tile), 128 (two tiles) or 32 (half a tile); 128
+// and 32 walk keys in ascending order only, 32 with bf16 Q and K.
+template <int RULE, int UNIT, int ORDER, bool Q8, int BC = kTK>
 __global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads),
                           amdgpu_waves_per_eu(2, 2))) void
 fa_fwd_kernel(FwdParams p) {
   static_assert(UNIT == kTQ || UNIT == 32, "decision unit is the tile or one wave");
+  static_assert(BC == kTK || BC == 2 * kTK || BC == kTK / 2, "B_c is 32, 64 or 128");
+  constexpr bool PAIR = BC == 2 * kTK;
+  constexpr bool HALF = BC == kTK / 2;
   __shared__ __attribute__((aligned(16))) Smem sm;
 
   const int tid = threadIdx.x;
@@ -864,7 +1076,7 @@ fa_fwd_kernel(FwdParams p) {
   const int unit_row0 = unit * UNIT;
   cx.rows_valid = max(0, min(UNIT, N - unit_row0));
   cx.mask_row = (p.mask != nullptr && cx.rows_valid > 0)
-                    ? p.mask + ((size_t)bh * p.n_qu + unit) * (PAIR ? p.n_kd : p.n_kt)
+                    ? p.mask + ((size_t)bh * p.n_qu + unit) * (BC == kTK ? p.n_kt : p.n_kd)
                     : nullptr;
   cx.diag_c = q0 / kTK;                               // < n_kt since q0 < N
   cx.diag_m = min(cx.diag_c, cx.n_kt - 1 - cx.diag_c);
@@ -927,7 +1139,18 @@ fa_fwd_kernel(FwdParams p) {
   SkipCount sk;
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");  // K_0 consumed
 
-  if constexpr (PAIR) {
+  if constexpr (HALF) {
+    static_assert(ORDER == kOrderAscending && !Q8, "32-key decisions: ascending, bf16");
+    float mh[2] = {block_max(sa[0]) * cx.c, block_max(sa[1]) * cx.c};
+    uint32_t votes[2] = {1u, 1u};            // h0 of the first tile is always kept
+    bool own[2] = {true, true};
+    for (int j = 0; j < cx.n_kt; j += 2) {
+      half_tile_step<RULE, UNIT>(j, sa, sb, mh, votes, own, v_ready, rs, o, qf, sm, cx, sk);
+      if (j + 1 < cx.n_kt)
+        half_tile_step<RULE, UNIT>(j + 1, sb, sa, mh, votes, own, v_ready, rs, o, qf, sm, cx,
+                                   sk);
+    }
+  } else if constexpr (PAIR) {
     static_assert(ORDER == kOrderAscending, "128-key decisions walk keys in ascending order");
     for (int j = 0; j < cx.n_kt; j += 2) {
       pair_first_step<RULE, UNIT, Q8>(j, sa, sb, mhat, keep_own, keep_any, v_ready, rs, o, qf,
@@ -952,7 +1175,7 @@ fa_fwd_kernel(FwdParams p) {
   if (p.stats != nullptr && (UNIT == kTQ ? cx.w == 0 : true) && cx.lane == 0 &&
       cx.rows_valid > 0) {
     unsigned long long* st = reinterpret_cast<unsigned long long*>(p.stats) + (size_t)bh * 4;
-    atomicAdd(st + 0, (unsigned long long)(PAIR ? p.n_kd : cx.n_kt));
+    atomicAdd(st + 0, (unsigned long long)(BC == kTK ? cx.n_kt : p.n_kd));
     atomicAdd(st + 1, (unsigned long long)sk.tiles);
     atomicAdd(st + 2, (unsigned long long)cx.rows_valid * (unsigned long long)N);
     atomicAdd(st + 3, (unsigned long long)sk.elems);
@@ -1200,16 +1423,38 @@ hipError_t launch_pair(int rule, const FwdParams& p, dim3 grid, hipStream_t stre
   const dim3 block(kThreads);
   switch (rule) {
     case kRuleDense:
-      hipLaunchKernelGGL((fa_fwd_kernel<kRuleDense, UNIT, kOrderAscending, Q8, true>), grid,
+      hipLaunchKernelGGL((fa_fwd_kernel<kRuleDense, UNIT, kOrderAscending, Q8, 2 * kTK>), grid,
                          block, 0, stream, p);
       break;
     case kRuleBlasst:
-      hipLaunchKernelGGL((fa_fwd_kernel<kRuleBlasst, UNIT, kOrderAscending, Q8, true>), grid,
+      hipLaunchKernelGGL((fa_fwd_kernel<kRuleBlasst, UNIT, kOrderAscending, Q8, 2 * kTK>), grid,
                          block, 0, stream, p);
       break;
     case kRuleDynSparse:
-      hipLaunchKernelGGL((fa_fwd_kernel<kRuleDynSparse, UNIT, kOrderAscending, Q8, true>), grid,
+      hipLaunchKernelGGL((fa_fwd_kernel<kRuleDynSparse, UNIT, kOrderAscending, Q8, 2 * kTK>), grid,
                          block, 0, stream, p);
+      break;
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <int UNIT>
+hipError_t launch_half(int rule, const FwdParams& p, dim3 grid, hipStream_t stream) {
+  const dim3 block(kThreads);
+  switch (rule) {
+    case kRuleDense:
+      hipLaunchKernelGGL((fa_fwd_kernel<kRuleDense, UNIT, kOrderAscending, false, kTK / 2>),
+                         grid, block, 0, stream, p);
+      break;
+    case kRuleBlasst:
+      hipLaunchKernelGGL((fa_fwd_kernel<kRuleBlasst, UNIT, kOrderAscending, false, kTK / 2>),
+                         grid, block, 0, stream, p);
+      break;
+    case kRuleDynSparse:
+      hipLaunchKernelGGL((fa_fwd_kernel<kRuleDynSparse, UNIT, kOrderAscending, false, kTK / 2>),
+                         grid, block, 0, stream, p);
       break;
     default:
       return hipErrorInvalidValue;
@@ -1222,6 +1467,10 @@ hipError_t launch_order(int rule, const FwdParams& p, dim3 grid, hipStream_t str
   if (p.key_tile == 2 * kTK) {
     if (p.key_order != kOrderAscending) return hipErrorInvalidValue;
     return launch_pair<UNIT, Q8>(rule, p, grid, stream);
+  }
+  if (p.key_tile == kTK / 2) {
+    if (p.key_order != kOrderAscending || Q8) return hipErrorInvalidValue;
+    return launch_half<UNIT>(rule, p, grid, stream);
   }
   if (p.key_order == kOrderDiagonal && rule != kRuleDense) {
     const int chunk = (p.n_qt + kXcds - 1) / kXcds;

@@ -103,7 +103,8 @@ def _fwd(name, param, B=1, H=1, N=128, d=128, scale=0.1, tq=128, tk=64, ptr=None
     ("blasst_attn_fwd", 1.1, {}, -1, "tau"),
     ("dynsparse_attn_fwd", 0.95, {"d": 64}, -2, "head dimension"),
     ("dynsparse_attn_fwd", 0.95, {"tq": 64}, -2, "tile"),
-    ("dynsparse_attn_fwd", 0.95, {"tq": 32, "tk": 32}, -2, "tile"),
+    ("dynsparse_attn_fwd", 0.95, {"tq": 32, "tk": 32}, -1, "non-null"),  # 32-key decisions pass
+    ("dynsparse_attn_fwd", 0.95, {"tq": 32, "tk": 16}, -2, "tile"),
     ("dynsparse_attn_fwd", 0.95, {"tq": 32}, -1, "non-null"),   # 32 x 64 passes the shape check
     ("dynsparse_attn_fwd", 0.95, {"tk": 128}, -1, "non-null"),  # 128-key decisions pass
     ("dynsparse_attn_fwd", 0.95, {"tk": 96}, -2, "tile"),
@@ -355,3 +356,9 @@ def test_key_tile_128_restrictions():
     a.param = 0.01
     assert L.dsattn_attn_fwd_ex(ctypes.byref(a)) == -1
     assert "non-null" in pkg.last_error()
+    a.tile_k, a.qk_format = 32, pkg.QK_MXFP8
+    assert L.dsattn_attn_fwd_ex(ctypes.byref(a)) == -2
+    assert "bf16" in pkg.last_error()
+    a.qk_format, a.key_order = 0, pkg.ORDER_DIAGONAL
+    assert L.dsattn_attn_fwd_ex(ctypes.byref(a)) == -2
+    assert "ascending" in pkg.last_error()
