@@ -878,29 +878,27 @@ __device__ __forceinline__ void qk_softmax_halves(const f32x16 (&s_cur)[2], floa
   __builtin_amdgcn_s_setprio(0);
 }
 
-// O += P V_j over the kept halves: MFMAs 0-7 cover keys 0-31, 8-15 keys 32-63.  va holds
-// the operands of MFMAs 0 and 1 on entry.
-__device__ __forceinline__ void pv_halves(f32x16 (&o)[4], const bf16x8 (&pf)[4], bf16x8 (&va)[3],
-                                          const uint16_t* vt, int lane, bool pv0, bool pv1) {
+// O += P V_j for the first key half (MFMAs 0-7, keys 0-31; va holds the operands of MFMAs
+// 0 and 1 on entry, those of 8 and 9 on exit) and for the second (MFMAs 8-15).
+__device__ __forceinline__ void pv_first_half(f32x16 (&o)[4], const bf16x8 (&pf)[4],
+                                              bf16x8 (&va)[3], const uint16_t* vt, int lane) {
   __builtin_amdgcn_s_setprio(1);
-  if (pv0) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      va[(i + 2) % 3] = v_operand(vt, i + 2, lane);
-      o[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i % 3], pf[i >> 2], o[i & 3], 0, 0, 0);
-      sched_fence();
-    }
-  } else {
-    va[8 % 3] = v_operand(vt, 8, lane);
-    va[9 % 3] = v_operand(vt, 9, lane);
+  for (int i = 0; i < 8; ++i) {
+    va[(i + 2) % 3] = v_operand(vt, i + 2, lane);
+    o[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i % 3], pf[i >> 2], o[i & 3], 0, 0, 0);
+    sched_fence();
   }
-  if (pv1) {
+  __builtin_amdgcn_s_setprio(0);
+}
+__device__ __forceinline__ void pv_second_half(f32x16 (&o)[4], const bf16x8 (&pf)[4],
+                                               bf16x8 (&va)[3], const uint16_t* vt, int lane) {
+  __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-    for (int i = 8; i < 16; ++i) {
-      if (i + 2 < 16) va[(i + 2) % 3] = v_operand(vt, i + 2, lane);
-      o[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i % 3], pf[i >> 2], o[i & 3], 0, 0, 0);
-      sched_fence();
-    }
+  for (int i = 8; i < 16; ++i) {
+    if (i + 2 < 16) va[(i + 2) % 3] = v_operand(vt, i + 2, lane);
+    o[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i % 3], pf[i >> 2], o[i & 3], 0, 0, 0);
+    sched_fence();
   }
   __builtin_amdgcn_s_setprio(0);
 }
@@ -950,10 +948,15 @@ __device__ __forceinline__ void half_tile_step(int j, const f32x16 (&s_cur)[2],
     keep1 = true;
     if (keep0) {
       rs.l_half += psum0;
+      bool own1 = true;
       if constexpr (RULE != kRuleDense) {
-        const bool own1 = __ballot(cx.valid & row_keeps<RULE>(rs, mh[1], cx.thr)) != 0;
+        own1 = __ballot(cx.valid & row_keeps<RULE>(rs, mh[1], cx.thr)) != 0;
+        if (UNIT == kTQ && cx.lane == 0) sm.vote_mid[cx.w] = own1 ? 1 : 0;
+      }
+      sched_fence();
+      pv_first_half(o, pf, va, sm.v[j & 1], cx.lane);   // under the vote exchange
+      if constexpr (RULE != kRuleDense) {
         if constexpr (UNIT == kTQ) {
-          if (cx.lane == 0) sm.vote_mid[cx.w] = own1 ? 1 : 0;
           asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
           keep1 = __builtin_amdgcn_readfirstlane(
                       *reinterpret_cast<const uint32_t*>(sm.vote_mid)) != 0;
@@ -961,13 +964,16 @@ __device__ __forceinline__ void half_tile_step(int j, const f32x16 (&s_cur)[2],
           keep1 = __builtin_amdgcn_readfirstlane((int)own1) != 0;
         }
       }
+    } else {
+      va[8 % 3] = v_operand(sm.v[j & 1], 8, cx.lane);
+      va[9 % 3] = v_operand(sm.v[j & 1], 9, cx.lane);
     }
     if (keep1) {
       rs.l_half += psum1;
       rs.m_true = fmaxf(rs.m_true, mh[1]);
+      sched_fence();
+      pv_second_half(o, pf, va, sm.v[j & 1], cx.lane);
     }
-    sched_fence();
-    pv_halves(o, pf, va, sm.v[j & 1], cx.lane, keep0, keep1);
   } else {
     skipped_tile(s_next, sm.k[nb], qf, cx.r, cx.g);
   }
