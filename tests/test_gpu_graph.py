@@ -1,0 +1,120 @@
+"""HIP graph capture of the C-ABI calls (torch.cuda.CUDAGraph over the library's kernels).
+
+The library clears stats_out with a fill kernel rather than a memset node, and allocates
+nothing, so a call can be captured and replayed.  Each graph is replayed several times
+with the program's own eager work and synchronisations in between and with new inputs
+copied into the captured buffers; every replay must equal an eager call on the same
+inputs bit for bit (the kernels are deterministic).
+"""
+
+import math
+import sys
+
+import numpy as np
+import pytest
+
+from synth import make_random_qkv, make_video_qkv
+
+from _parity import to_device
+
+pytestmark = pytest.mark.gpu
+
+SCALE = 1.0 / math.sqrt(128)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2606_16317_amd as dsa
+
+    dsa.lib()
+    return torch
+
+
+def announce(msg):
+    print(f"\n[case] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+def buffers(B, H, N, tile_q=128, tile_k=64):
+    import torch
+
+    n_qt, n_kt = -(-N // tile_q), -(-N // tile_k)
+    return (torch.empty((B, H, N, 128), dtype=torch.bfloat16, device="cuda"),
+            torch.zeros(B * H * 4, dtype=torch.int64, device="cuda"),
+            torch.zeros(B * H * n_qt * n_kt, dtype=torch.uint8, device="cuda"),
+            torch.zeros(B * H * N, dtype=torch.float32, device="cuda"))
+
+
+@pytest.mark.parametrize("rule,param,tile_q,tile_k", [(3, -6.0, 128, 64), (1, 1e-2, 32, 64),
+                                                      (0, 0.0, 128, 64), (3, -6.0, 128, 128),
+                                                      (2, 0.9, 128, 32)])
+def test_attention_call_replays_match_eager(rule, param, tile_q, tile_k):
+    import torch
+    import paper_2606_16317_amd as dsa
+
+    announce(f"graph rule={rule} param={param} tile_q={tile_q} tile_k={tile_k}")
+    B, H, N = 1, 3, 1000
+    inputs = [make_video_qkv(B, H, (2, 10, 50), 4.0, 4.0, True, s)[:3] for s in (1, 2, 3)]
+    qd, kd, vd = (to_device(x) for x in inputs[0])
+    o, st, mk, ls = buffers(B, H, N, tile_q, tile_k)
+
+    def call(q, k, v, o, st, mk, ls):
+        dsa.dsattn_attn_fwd_ex(rule, param, q, k, v, o, scale=SCALE, tile_q=tile_q,
+                               tile_k=tile_k, stats_out=st, mask_out=mk, lse_out=ls)
+
+    call(qd, kd, vd, o, st, mk, ls)                      # warm-up outside the capture
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        call(qd, kd, vd, o, st, mk, ls)
+    for rep in range(4):
+        q, k, v = inputs[rep % 3]
+        qd.copy_(to_device(q)); kd.copy_(to_device(k)); vd.copy_(to_device(v))
+        st.fill_(-1); mk.fill_(9); o.zero_()
+        g.replay()
+        ref = buffers(B, H, N, tile_q, tile_k)
+        call(to_device(q), to_device(k), to_device(v), *ref)   # eager, other buffers
+        torch.cuda.synchronize()
+        for got, want in zip((o, st, mk, ls), ref):
+            assert torch.equal(got, want), rep
+
+
+def test_quantise_and_q8_attention_replays_match_eager():
+    import torch
+    import paper_2606_16317_amd as dsa
+
+    announce("graph quantise + mxfp8 attention")
+    B, H, N = 1, 2, 777
+    q, k, v = make_random_qkv(B, H, N, 128, 11, q_std=2.0, k_std=2.0)
+    qd, kd, vd = to_device(q), to_device(k), to_device(v)
+    qc = torch.empty((B, H, N, 128), dtype=torch.uint8, device="cuda")
+    kc = torch.empty_like(qc)
+    qs = torch.empty((B, H, N, 4), dtype=torch.uint8, device="cuda")
+    ks = torch.empty_like(qs)
+    mean = torch.empty((B, H, 128), dtype=torch.float32, device="cuda")
+    o, st, mk, ls = buffers(B, H, N)
+
+    def pipeline(o, st, mk, ls):
+        dsa.dsattn_quantize_mxfp8(qd, qc, qs)
+        dsa.dsattn_key_mean(kd, mean)
+        dsa.dsattn_quantize_mxfp8(kd, kc, ks, shift=mean)
+        dsa.dsattn_attn_fwd_mxfp8(3, -4.0, qc, qs, kc, ks, vd, o, scale=SCALE, stats_out=st,
+                                  mask_out=mk, lse_out=ls)
+
+    pipeline(o, st, mk, ls)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        pipeline(o, st, mk, ls)
+    for rep in range(3):
+        kd.mul_(1.5 if rep % 2 else 0.75)                 # new keys each replay
+        g.replay()
+        torch.cuda.synchronize()
+        got = [t.clone() for t in (o, st, mk, ls)]
+        pipeline(o, st, mk, ls)                           # eager on the same inputs
+        torch.cuda.synchronize()
+        for a, b in zip(got, (o, st, mk, ls)):
+            assert torch.equal(a, b), rep
