@@ -1,8 +1,8 @@
 // Tile-filtered FlashAttention forward kernels for gfx950 (CDNA4).
 //
 // One workgroup computes one (b, h, query tile of 128 rows); its four waves own 32 query
-// rows each.  Key tiles of 64 keys are visited in ascending order (Section 1, tile-based
-// attention).  For every tile the kernel
+// rows each.  Key tiles of 64 keys are visited in ascending order by default (Section 1,
+// tile-based attention).  For every tile the kernel
 //
 //   1. computes S^T = K_j Q_i^T on MFMA (bf16 inputs, fp32 accumulation) -- always;
 //   2. takes the per-row tile maximum m_hat -- always;
@@ -25,12 +25,22 @@
 //
 // Pipeline (one barrier per key tile): S_{j+1} is computed during iteration j, so the
 // decision for tile j+1 is voted before the barrier that closes iteration j and read
-// right after it (the read's latency overlaps the issue of the next K-tile DMA).  K is prefetched two tiles ahead and V one tile ahead, straight from
-// global memory into LDS (buffer loads with the LDS bit; rows past the sequence end come
-// back as zeros from the buffer range check); V is fetched only for tiles that follow a
-// kept tile or are themselves kept, so runs of skipped tiles stream K alone.  Inside an iteration the instruction
-// order is fixed by scheduling fences: each of the 16 S_{j+1} MFMAs carries two
-// elements of the tile-j softmax, and MFMA operands are read from LDS two MFMAs ahead.
+// right after it (the read's latency overlaps the issue of the next K-tile DMA).  K is
+// prefetched two tiles ahead and V one tile ahead, straight from global memory into LDS
+// (buffer loads with the LDS bit; rows past the sequence end come back as zeros from the
+// buffer range check); V is fetched only for tiles that follow a kept tile or are
+// themselves kept, so runs of skipped tiles stream K alone.  Inside an iteration the
+// instruction order is fixed by scheduling fences: each of the 16 S_{j+1} MFMAs carries
+// two elements of the tile-j softmax, and MFMA operands are read from LDS two MFMAs
+// ahead.
+//
+// Variants, all compile-time parameters of fa_fwd_kernel:
+//   * UNIT: the query rows that share a decision, the workgroup's 128 or each wave's 32;
+//   * ORDER: key tiles in ascending or diagonal-first order;
+//   * Q8: Q and K in MX-FP8 on the scaled fp8 MFMA (the rest of the tile is unchanged);
+//   * BC: keys per decision, 64 (one tile), 128 (two tiles deciding together) or 32 (the
+//     halves of each tile deciding in turn).
+// fa_fwd_mask_kernel applies a given skip mask instead of a rule (mask reuse).
 //
 // Online softmax uses a lazily updated reference max m_ref: O and l are rescaled only
 // when a kept tile's max exceeds m_ref by more than 8 (log2 units), so P <= 2^8.  The
