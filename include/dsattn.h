@@ -27,7 +27,7 @@
  *   key tile B_c, the number of keys one skip decision covers (Section 4.2.1 uses 128 for
  *   the 14B model and 32 for the 5B model).  The kernels work on 64-key tiles: 128 is two
  *   of them deciding together, 32 their two halves deciding in turn; both visit keys in
- *   ascending order only, 32 with bf16 q and k; tile_q is the number of query rows that share one skip
+ *   ascending order only; tile_q is the number of query rows that share one skip
  *   decision ("query tile" below): 128 decides per workgroup tile, 32 lets every 32-row
  *   slice decide on its own (a finer granularity of the same rule, which the paper
  *   leaves open).  B, H,

@@ -86,8 +86,6 @@ int check_problem(const dsattn_args& a) {
                   a.tile_k);
     if (a.rule == DSATTN_RULE_MASK)
       return fail(DSATTN_EUNSUPPORTED, "mask reuse takes tile_k = 64");
-    if (a.tile_k == kTileKHalf && a.qk_format != DSATTN_QK_BF16)
-      return fail(DSATTN_EUNSUPPORTED, "tile_k = 32 takes bf16 q and k");
   }
   if (a.rule == DSATTN_RULE_MASK) {
     if (a.key_order != DSATTN_ORDER_ASCENDING)

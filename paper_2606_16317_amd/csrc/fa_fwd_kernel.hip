@@ -888,6 +888,35 @@ __device__ __forceinline__ void qk_softmax_halves(const f32x16 (&s_cur)[2], floa
   __builtin_amdgcn_s_setprio(0);
 }
 
+// The same on the MX-FP8 path: the four scaled MFMAs of S_{j+1} carry eight elements
+// each, the first two h0's and the last two h1's.
+__device__ __forceinline__ void qk_softmax_halves_q8(const f32x16 (&s_cur)[2], float c,
+                                                     float neg_m0, float neg_m1, float& psum0,
+                                                     float& psum1, bf16x8 (&pf)[4],
+                                                     bf16x8 (&va)[3], f32x16 (&s_next)[2],
+                                                     const uint8_t* kt, const uint8_t* ks,
+                                                     const uint16_t* vt, const QFrag8& qf,
+                                                     int r, int g, int lane) {
+  KFrag8 kf;
+  k8_begin(kf, kt, ks, r, g);
+  sched_fence();
+  __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    qk_q8_step(i, s_next, kf, kt, qf, r, g);
+    if (i >= 2) va[i - 2] = v_operand(vt, i - 2, lane);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      if (i < 2)
+        softmax_elem(s_cur, 8 * i + e, c, neg_m0, psum0, pf);
+      else
+        softmax_elem(s_cur, 8 * i + e, c, neg_m1, psum1, pf);
+    }
+    sched_fence();
+  }
+  __builtin_amdgcn_s_setprio(0);
+}
+
 // O += P V_j for the first key half (MFMAs 0-7, keys 0-31; va holds the operands of MFMAs
 // 0 and 1 on entry, those of 8 and 9 on exit) and for the second (MFMAs 8-15).
 __device__ __forceinline__ void pv_first_half(f32x16 (&o)[4], const bf16x8 (&pf)[4],
@@ -917,16 +946,16 @@ __device__ __forceinline__ void pv_second_half(f32x16 (&o)[4], const bf16x8 (&pf
 // maxima (log2 units); vote[0] / vote[1] are the workgroup's vote words for h0 and for h1
 // against the same LSE (used for h1 when h0 is skipped), own[0] / own[1] this wave's own
 // votes (the decisions of 32-row units).  On exit the same for tile j+1.
-template <int RULE, int UNIT>
+template <int RULE, int UNIT, bool Q8>
 __device__ __forceinline__ void half_tile_step(int j, const f32x16 (&s_cur)[2],
                                                f32x16 (&s_next)[2], float (&mh)[2],
                                                uint32_t (&vote)[2], bool (&own)[2],
                                                bool& v_ready, RowState& rs, f32x16 (&o)[4],
-                                               const bf16x8 (&qf)[8], Smem& sm,
-                                               const LoopCtx& cx, SkipCount& sk) {
+                                               const typename QFragOf<Q8>::type& qf,
+                                               Smem& sm, const LoopCtx& cx, SkipCount& sk) {
   const int nb = (j + 1) & 1;
   const bool has_next = (j + 1) < cx.n_kt;
-  load_tile_lds(sm.k[j & 1], cx.krs, cx.koff, (j + 2) * kTK, cx.w);
+  load_k_tile<Q8>(sm, j & 1, cx, (j + 2) * kTK);
   bool keep0 = true, keep1_pre = true, need_v = true;
   if constexpr (RULE != kRuleDense) {
     const bool any0 = __builtin_amdgcn_readfirstlane(vote[0]) != 0;
@@ -952,8 +981,14 @@ __device__ __forceinline__ void half_tile_step(int j, const f32x16 (&s_cur)[2],
     // relative to -inf in the second case.
     raise_reference(rs, o, keep0 ? fmaxf(mh[0], mh[1]) : mh[1]);
     if (keep0) rs.m_true = fmaxf(rs.m_true, mh[0]);
-    qk_softmax_halves(s_cur, cx.c, keep0 ? -rs.m_ref : -__builtin_inff(), -rs.m_ref, psum0,
-                      psum1, pf, va, s_next, sm.k[nb], sm.v[j & 1], qf, cx.r, cx.g, cx.lane);
+    if constexpr (Q8)
+      qk_softmax_halves_q8(s_cur, cx.c, keep0 ? -rs.m_ref : -__builtin_inff(), -rs.m_ref,
+                           psum0, psum1, pf, va, s_next,
+                           reinterpret_cast<const uint8_t*>(sm.k[nb]), sm.ks[nb], sm.v[j & 1],
+                           qf, cx.r, cx.g, cx.lane);
+    else
+      qk_softmax_halves(s_cur, cx.c, keep0 ? -rs.m_ref : -__builtin_inff(), -rs.m_ref, psum0,
+                        psum1, pf, va, s_next, sm.k[nb], sm.v[j & 1], qf, cx.r, cx.g, cx.lane);
     sched_fence();
     keep1 = true;
     if (keep0) {
@@ -985,7 +1020,11 @@ __device__ __forceinline__ void half_tile_step(int j, const f32x16 (&s_cur)[2],
       pv_second_half(o, pf, va, sm.v[j & 1], cx.lane);
     }
   } else {
-    skipped_tile(s_next, sm.k[nb], qf, cx.r, cx.g);
+    if constexpr (Q8)
+      skipped_tile_q8(s_next, reinterpret_cast<const uint8_t*>(sm.k[nb]), sm.ks[nb], qf, cx.r,
+                      cx.g);
+    else
+      skipped_tile(s_next, sm.k[nb], qf, cx.r, cx.g);
   }
   keep1 = keep1 && h1_exists;
   if (cx.mask_row != nullptr && (UNIT == kTQ ? cx.w == 0 : true) && cx.lane == 0) {
@@ -1032,7 +1071,7 @@ __device__ __forceinline__ void half_tile_step(int j, const f32x16 (&s_cur)[2],
 // Q8: Q and K in MX-FP8 (codes p.q8 / p.k8, exponents p.q_scales / p.k_scales), S = Q K^T
 // on the scaled fp8 MFMA; everything after S is the same as with bf16 Q and K.
 // BC: keys per skip decision: 64 (one tile), 128 (two tiles) or 32 (half a tile); 128
-// and 32 walk keys in ascending order only, 32 with bf16 Q and K.
+// and 32 walk keys in ascending order only.
 template <int RULE, int UNIT, int ORDER, bool Q8, int BC = kTK>
 __global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads),
                           amdgpu_waves_per_eu(2, 2))) void
@@ -1156,15 +1195,16 @@ fa_fwd_kernel(FwdParams p) {
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");  // K_0 consumed
 
   if constexpr (HALF) {
-    static_assert(ORDER == kOrderAscending && !Q8, "32-key decisions: ascending, bf16");
+    static_assert(ORDER == kOrderAscending, "32-key decisions walk keys in ascending order");
     float mh[2] = {block_max(sa[0]) * cx.c, block_max(sa[1]) * cx.c};
     uint32_t votes[2] = {1u, 1u};            // h0 of the first tile is always kept
     bool own[2] = {true, true};
     for (int j = 0; j < cx.n_kt; j += 2) {
-      half_tile_step<RULE, UNIT>(j, sa, sb, mh, votes, own, v_ready, rs, o, qf, sm, cx, sk);
+      half_tile_step<RULE, UNIT, Q8>(j, sa, sb, mh, votes, own, v_ready, rs, o, qf, sm, cx,
+                                     sk);
       if (j + 1 < cx.n_kt)
-        half_tile_step<RULE, UNIT>(j + 1, sb, sa, mh, votes, own, v_ready, rs, o, qf, sm, cx,
-                                   sk);
+        half_tile_step<RULE, UNIT, Q8>(j + 1, sb, sa, mh, votes, own, v_ready, rs, o, qf, sm,
+                                       cx, sk);
     }
   } else if constexpr (PAIR) {
     static_assert(ORDER == kOrderAscending, "128-key decisions walk keys in ascending order");
@@ -1456,20 +1496,20 @@ hipError_t launch_pair(int rule, const FwdParams& p, dim3 grid, hipStream_t stre
   return hipGetLastError();
 }
 
-template <int UNIT>
+template <int UNIT, bool Q8>
 hipError_t launch_half(int rule, const FwdParams& p, dim3 grid, hipStream_t stream) {
   const dim3 block(kThreads);
   switch (rule) {
     case kRuleDense:
-      hipLaunchKernelGGL((fa_fwd_kernel<kRuleDense, UNIT, kOrderAscending, false, kTK / 2>),
-                         grid, block, 0, stream, p);
+      hipLaunchKernelGGL((fa_fwd_kernel<kRuleDense, UNIT, kOrderAscending, Q8, kTK / 2>), grid,
+                         block, 0, stream, p);
       break;
     case kRuleBlasst:
-      hipLaunchKernelGGL((fa_fwd_kernel<kRuleBlasst, UNIT, kOrderAscending, false, kTK / 2>),
-                         grid, block, 0, stream, p);
+      hipLaunchKernelGGL((fa_fwd_kernel<kRuleBlasst, UNIT, kOrderAscending, Q8, kTK / 2>), grid,
+                         block, 0, stream, p);
       break;
     case kRuleDynSparse:
-      hipLaunchKernelGGL((fa_fwd_kernel<kRuleDynSparse, UNIT, kOrderAscending, false, kTK / 2>),
+      hipLaunchKernelGGL((fa_fwd_kernel<kRuleDynSparse, UNIT, kOrderAscending, Q8, kTK / 2>),
                          grid, block, 0, stream, p);
       break;
     default:
@@ -1485,8 +1525,8 @@ hipError_t launch_order(int rule, const FwdParams& p, dim3 grid, hipStream_t str
     return launch_pair<UNIT, Q8>(rule, p, grid, stream);
   }
   if (p.key_tile == kTK / 2) {
-    if (p.key_order != kOrderAscending || Q8) return hipErrorInvalidValue;
-    return launch_half<UNIT>(rule, p, grid, stream);
+    if (p.key_order != kOrderAscending) return hipErrorInvalidValue;
+    return launch_half<UNIT, Q8>(rule, p, grid, stream);
   }
   if (p.key_order == kOrderDiagonal && rule != kRuleDense) {
     const int chunk = (p.n_qt + kXcds - 1) / kXcds;

@@ -8,7 +8,7 @@ the previous pair); with 32 it decides for the two halves of every 64-key tile i
 decisions (mismatches only within the 1e-3 margin), outputs and LSE within the same
 tolerances, stats implied by the mask, the recall bound of Section 3.1 from the GPU's own
 LSE, ragged sequences (a last 128-key tile with one 64-key tile or a partial one, a last
-64-key tile with no second half), both decision units, and MX-FP8 Q and K at 128.
+64-key tile with no second half), both decision units, and MX-FP8 Q and K.
 """
 
 import math
@@ -154,34 +154,35 @@ def test_finer_key_tiles_skip_more(peaked):
     assert 0.0 < sp[128] <= sp[64] <= sp[32]
 
 
+@pytest.mark.parametrize("tk", KEY_TILES)
 @pytest.mark.parametrize("rule,param", [("dynsparse_lambda", -6.0), ("blasst", 1e-2),
                                         ("dense", 0.0)])
-def test_mxfp8_with_128_key_decisions(peaked, rule, param):
+def test_mxfp8_with_key_tiles(peaked, tk, rule, param):
     import torch
     import paper_2606_16317_amd as dsa
 
     (q, k, v), dev = peaked
-    announce(f"tile_k=128 mxfp8 rule={rule} param={param}")
+    announce(f"tile_k={tk} mxfp8 rule={rule} param={param}")
     qc, qs = quantize_mxfp8(oracle.bf16_to_f64(q))
     kc, ks = quantize_mxfp8(oracle.bf16_to_f64(k))
     up = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
     B, H, N, d = q.shape
-    n_kd = -(-N // TK)
+    n_kd = -(-N // tk)
     o = torch.empty_like(dev[2])
     stats = torch.full((B * H * 4,), -7, dtype=torch.int64, device="cuda")
     mask = torch.full((B * H * (N // 128) * n_kd,), 7, dtype=torch.uint8, device="cuda")
     lse = torch.full((B * H * N,), float("nan"), dtype=torch.float32, device="cuda")
     dsa.dsattn_attn_fwd_mxfp8(RULE_NAMES[rule], param, up(qc), up(qs), up(kc), up(ks), dev[2],
-                              o, scale=SCALE, tile_k=TK, stats_out=stats, mask_out=mask,
+                              o, scale=SCALE, tile_k=tk, stats_out=stats, mask_out=mask,
                               lse_out=lse)
     torch.cuda.synchronize()
     g = GpuRun(from_device_bf16(o), mask.cpu().numpy().reshape(B, H, N // 128, n_kd),
                lse.cpu().numpy().reshape(B, H, N), stats.cpu().numpy().reshape(B, H, 4))
     rep = compare(dequantize_mxfp8(qc, qs), dequantize_mxfp8(kc, ks), v, g, rule, param, SCALE,
-                  tile_k=TK, tiles=sample_tiles(B, H, N, per_head=4, seed=2))
+                  tile_k=tk, tiles=sample_tiles(B, H, N, per_head=4, seed=2))
     print(rep, flush=True)
     assert_parity(rep)
-    assert (g.stats == expected_stats_from_mask(g.mask, N, 128, TK)).all()
+    assert (g.stats == expected_stats_from_mask(g.mask, N, 128, tk)).all()
 
 
 @pytest.mark.parametrize("tk", KEY_TILES)
