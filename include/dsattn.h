@@ -167,10 +167,11 @@ int dsattn_attn_fwd_ex(const dsattn_args* args);
  * nonzero = skip), and the output is attention over the kept key tiles, renormalised as
  * for the rules.  Skipped tiles cost nothing, not even Q K^T: each workgroup visits only
  * the tiles one of its rows keeps, in ascending order.  A unit that keeps no tile gets
- * zeros and an LSE of -inf.  Reusing the mask a rule call wrote (same inputs, tile_q and
- * ascending order) reproduces that call's output bit for bit.  Requirements: mask_in
- * non-NULL, key_order ascending, ceil(N/tile_k) <= 4096 (N <= 262144), else
- * DSATTN_EINVAL / DSATTN_EUNSUPPORTED.  mask_out, if given, receives mask_in (as 0/1).
+ * zeros and an LSE of -inf.  Reusing the mask a rule call wrote with tile_k = 64 (same
+ * inputs, tile_q and ascending order) reproduces that call's output bit for bit.  tile_k
+ * may be 64 or 128 (a 128-key decision keeps or skips two 64-key tiles).  Requirements:
+ * mask_in non-NULL, key_order ascending, N <= 262144, else DSATTN_EINVAL /
+ * DSATTN_EUNSUPPORTED.  mask_out, if given, receives mask_in (as 0/1).
  */
 
 /*

@@ -262,7 +262,7 @@ def dsattn_attn_fwd_ex(rule, param, q, k, v, o=None, scale=None, tile_q=TILE_Q,
     mi = None
     if mask_in is not None:
         n_qu = -(-N // max(1, tile_q))
-        mi = _ptr(mask_in, B * H * n_qu * (-(-N // TILE_K)), (torch.uint8,), "mask_in")
+        mi = _ptr(mask_in, B * H * n_qu * (-(-N // max(1, tile_k))), (torch.uint8,), "mask_in")
     a = DsAttnArgs(rule, param, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
                    B, H, N, d, scale, tile_q, tile_k, _stream(stream), st, mk, ls, key_order,
                    mi)

@@ -84,8 +84,8 @@ int check_problem(const dsattn_args& a) {
     if (a.key_order != DSATTN_ORDER_ASCENDING)
       return fail(DSATTN_EUNSUPPORTED, "tile_k = %d visits key tiles in ascending order only",
                   a.tile_k);
-    if (a.rule == DSATTN_RULE_MASK)
-      return fail(DSATTN_EUNSUPPORTED, "mask reuse takes tile_k = 64");
+    if (a.rule == DSATTN_RULE_MASK && a.tile_k != kTileKPair)
+      return fail(DSATTN_EUNSUPPORTED, "mask reuse takes tile_k = 64 or 128");
   }
   if (a.rule == DSATTN_RULE_MASK) {
     if (a.key_order != DSATTN_ORDER_ASCENDING)

@@ -1242,7 +1242,8 @@ fa_fwd_kernel(FwdParams p) {
 // A skip mask from an earlier call (for instance an earlier denoising step of the same
 // layer) is applied as given: the workgroup visits only the key tiles some of its units
 // keep, in ascending order; a unit that skips a visited tile (UNIT = 32) adds nothing for
-// it.  Tiles nobody keeps cost nothing at all, not even QK^T.
+// it.  Tiles nobody keeps cost nothing at all, not even QK^T.  A mask of 128-key
+// decisions keeps or skips both 64-key tiles of each decision.
 
 // Visited tiles of one workgroup, ascending: (key tile << 4) | keep bit of each wave.
 __device__ __forceinline__ int list_tile(const MaskSmem& sm, int s) {
@@ -1329,17 +1330,21 @@ fa_fwd_mask_kernel(FwdParams p) {
 #pragma unroll
   for (int u = 0; u < kTQ / 32; ++u) {
     const int uu = UNIT == kTQ ? qt : qt * (kTQ / UNIT) + u;
-    rows[u] = (u < n_units && uu * UNIT < N) ? p.mask_in + ((size_t)bh * p.n_qu + uu) * p.n_kt
+    rows[u] = (u < n_units && uu * UNIT < N) ? p.mask_in + ((size_t)bh * p.n_qu + uu) * p.n_kd
                                              : nullptr;
   }
+  // Mask columns are decisions of key_tile keys: 64-key tile t reads column t (64) or
+  // t / 2 (128, two tiles per decision).
+  const int col_shift = p.key_tile == 2 * kTK ? 1 : 0;
   auto keep_bits = [&](int t) -> uint32_t {
+    const int col = t >> col_shift;
     if constexpr (UNIT == kTQ) {
-      return rows[0][t] == 0 ? 0xFu : 0u;
+      return rows[0][col] == 0 ? 0xFu : 0u;
     } else {
       uint32_t b = 0;
 #pragma unroll
       for (int u = 0; u < kTQ / 32; ++u)
-        if (rows[u] != nullptr && rows[u][t] == 0) b |= 1u << u;
+        if (rows[u] != nullptr && rows[u][col] == 0) b |= 1u << u;
       return b;
     }
   };
@@ -1373,17 +1378,17 @@ fa_fwd_mask_kernel(FwdParams p) {
     for (int u = 0; u < n_units; ++u) {
       if (rows[u] == nullptr) continue;
       const int uu = UNIT == kTQ ? qt : qt * (kTQ / UNIT) + u;
-      uint8_t* out = p.mask + ((size_t)bh * p.n_qu + uu) * p.n_kt;
-      for (int t = tid; t < cx.n_kt; t += kThreads) out[t] = rows[u][t] != 0 ? 1 : 0;
+      uint8_t* out = p.mask + ((size_t)bh * p.n_qu + uu) * p.n_kd;
+      for (int t = tid; t < p.n_kd; t += kThreads) out[t] = rows[u][t] != 0 ? 1 : 0;
     }
   }
   if (p.stats != nullptr && (UNIT == kTQ ? cx.w == 0 : true) && cx.rows_valid > 0) {
     const uint8_t* own = rows[UNIT == kTQ ? 0 : cx.w];
     uint32_t skipped = 0, width = 0;
-    for (int t = cx.lane; t < cx.n_kt; t += 64)
+    for (int t = cx.lane; t < p.n_kd; t += 64)
       if (own[t] != 0) {
         skipped += 1;
-        width += (uint32_t)min(kTK, N - t * kTK);
+        width += (uint32_t)min(p.key_tile, N - t * p.key_tile);
       }
 #pragma unroll
     for (int sh = 32; sh >= 1; sh >>= 1) {
@@ -1392,7 +1397,7 @@ fa_fwd_mask_kernel(FwdParams p) {
     }
     if (cx.lane == 0) {
       unsigned long long* st = reinterpret_cast<unsigned long long*>(p.stats) + (size_t)bh * 4;
-      atomicAdd(st + 0, (unsigned long long)cx.n_kt);
+      atomicAdd(st + 0, (unsigned long long)p.n_kd);
       atomicAdd(st + 1, (unsigned long long)skipped);
       atomicAdd(st + 2, (unsigned long long)cx.rows_valid * (unsigned long long)N);
       atomicAdd(st + 3, (unsigned long long)cx.rows_valid * (unsigned long long)width);

@@ -350,8 +350,12 @@ def test_key_tile_128_restrictions():
     assert L.dsattn_attn_fwd_ex(ctypes.byref(a)) == -2
     assert "ascending" in pkg.last_error()
     a.key_order, a.rule = pkg.ORDER_ASCENDING, pkg.RULE_MASK
+    assert L.dsattn_attn_fwd_ex(ctypes.byref(a)) == -1      # 128-key masks are reusable
+    assert "mask_in" in pkg.last_error() or "non-null" in pkg.last_error()
+    a.tile_k = 32
     assert L.dsattn_attn_fwd_ex(ctypes.byref(a)) == -2
-    assert "tile_k = 64" in pkg.last_error()
+    assert "tile_k = 64 or 128" in pkg.last_error()
+    a.tile_k = 128
     a.rule = pkg.RULE_BLASST
     a.param = 0.01
     assert L.dsattn_attn_fwd_ex(ctypes.byref(a)) == -1
