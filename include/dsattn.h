@@ -30,9 +30,9 @@
  *   ascending order only; tile_q is the number of query rows that share one skip
  *   decision ("query tile" below): 128 decides per workgroup tile, 32 lets every 32-row
  *   slice decide on its own (a finer granularity of the same rule, which the paper
- *   leaves open).  B, H,
- *   N >= 0 and B*H <= 65535; B == 0, H == 0 or N == 0 is an empty problem: nothing is
- *   read or written except stats_out, which is zeroed.
+ *   leaves open).  B, H, N >= 0, N <= 8388607 and B*H <= 65535; B == 0, H == 0 or
+ *   N == 0 is an empty problem: nothing is read or written except stats_out, which is
+ *   zeroed.
  * Memory: every pointer is a device pointer allocated by the caller on the current HIP
  *   device; the library never allocates, frees or retains memory.  q, k, v are read-only;
  *   o must not alias q, k or v; q, k, v, o must be 16-byte aligned and lse_out 4-byte

@@ -74,6 +74,11 @@ int check_problem(const dsattn_args& a) {
   if (bh > 65535) return fail(DSATTN_EINVAL, "B*H must be <= 65535 (got %lld)", bh);
   if ((long long)a.N * kHeadDim * bh > (1LL << 40))
     return fail(DSATTN_EINVAL, "problem too large");
+  // The kernels address one head's keys and values (N rows of 256 bytes) through a
+  // 32-bit buffer range.
+  if ((long long)a.N * kHeadDim * 2 > INT32_MAX)
+    return fail(DSATTN_EINVAL, "N must be <= %d (got %d)", (int)(INT32_MAX / (kHeadDim * 2)),
+                a.N);
   if (a.key_order != DSATTN_ORDER_ASCENDING && a.key_order != DSATTN_ORDER_DIAGONAL)
     return fail(DSATTN_EINVAL, "unknown key order %d", a.key_order);
   if (a.qk_format != DSATTN_QK_BF16 && a.qk_format != DSATTN_QK_MXFP8)

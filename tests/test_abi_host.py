@@ -109,6 +109,8 @@ def _fwd(name, param, B=1, H=1, N=128, d=128, scale=0.1, tq=128, tk=64, ptr=None
     ("dynsparse_attn_fwd", 0.95, {"tk": 128}, -1, "non-null"),  # 128-key decisions pass
     ("dynsparse_attn_fwd", 0.95, {"tk": 96}, -2, "tile"),
     ("dynsparse_attn_fwd", 0.95, {"N": -1}, -1, ">= 0"),
+    ("dynsparse_attn_fwd", 0.95, {"N": 8388608}, -1, "N must be <= 8388607"),
+    ("dynsparse_attn_fwd", 0.95, {"N": 8388607}, -1, "non-null"),   # the largest N passes
     ("dynsparse_attn_fwd", 0.95, {"B": -2}, -1, ">= 0"),
     ("dynsparse_attn_fwd", 0.95, {"scale": 0.0}, -1, "scale"),
     ("dynsparse_attn_fwd", 0.95, {"scale": float("inf")}, -1, "scale"),
