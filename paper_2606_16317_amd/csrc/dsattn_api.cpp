@@ -510,7 +510,8 @@ int quantize(const void* src, const float* shift, void* codes, void* scales, lon
     return fail(DSATTN_EINVAL, "group_rows must be > 0 (got %lld)", group_rows);
   const long long n_blocks = rows * (row_len / 32);
   if (rows > 0 && n_blocks / rows != row_len / 32) return fail(DSATTN_EINVAL, "problem too large");
-  if (n_blocks > (1LL << 40)) return fail(DSATTN_EINVAL, "problem too large");
+  // one thread per block, 256 per workgroup: keep the grid far inside its 2^31 limit
+  if (n_blocks > (1LL << 36)) return fail(DSATTN_EINVAL, "problem too large");
   if (n_blocks == 0) {
     g_last_error.clear();
     return DSATTN_OK;
