@@ -35,7 +35,8 @@
  *   zeroed.
  * Memory: every pointer is a device pointer allocated by the caller on the current HIP
  *   device; the library never allocates, frees or retains memory.  q, k, v are read-only;
- *   o must not alias q, k or v; q, k, v, o must be 16-byte aligned and lse_out 4-byte
+ *   the outputs (o, lse_out, mask_out, stats_out) must not overlap any input or each
+ *   other (checked on byte ranges); q, k, v, o must be 16-byte aligned and lse_out 4-byte
  *   aligned.
  * Execution: asynchronous on `stream` (0 = the null stream).  Argument errors are found
  *   on the host before anything is enqueued.  Calls that share output buffers on one

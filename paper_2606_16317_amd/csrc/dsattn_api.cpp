@@ -104,6 +104,53 @@ int check_problem(const dsattn_args& a) {
 
 bool empty_problem(const dsattn_args& a) { return a.B == 0 || a.H == 0 || a.N == 0; }
 
+// Byte ranges of the buffers one call reads and writes.
+struct Span {
+  const char* name;
+  uintptr_t lo, hi;   // [lo, hi); empty when the buffer is absent
+};
+
+Span span(const char* name, const void* p, size_t bytes) {
+  const uintptr_t lo = reinterpret_cast<uintptr_t>(p);
+  return Span{name, lo, p == nullptr ? lo : lo + bytes};
+}
+
+bool overlap(const Span& x, const Span& y) {
+  return x.lo < x.hi && y.lo < y.hi && x.lo < y.hi && y.lo < x.hi;
+}
+
+// Every output must be disjoint from every input and from the other outputs (the kernels
+// read inputs while writing outputs, from many workgroups at once).
+int check_overlaps(const dsattn_args& a) {
+  const size_t rows = (size_t)a.B * (size_t)a.H * (size_t)a.N;
+  const bool q8 = a.qk_format == DSATTN_QK_MXFP8;
+  const size_t qk_bytes = rows * (size_t)kHeadDim * (q8 ? 1 : 2);
+  const size_t units = (size_t)a.B * (size_t)a.H * (size_t)((a.N + a.tile_q - 1) / a.tile_q);
+  const size_t mask_bytes = units * (size_t)((a.N + a.tile_k - 1) / a.tile_k);
+  const Span in[] = {
+      span("q", a.q, qk_bytes),
+      span("k", a.k, qk_bytes),
+      span("v", a.v, rows * kHeadDim * 2),
+      span("q_scales", q8 ? a.q_scales : nullptr, rows * 4),
+      span("k_scales", q8 ? a.k_scales : nullptr, rows * 4),
+      span("mask_in", a.rule == DSATTN_RULE_MASK ? a.mask_in : nullptr, mask_bytes),
+  };
+  const Span out[] = {
+      span("o", a.o, rows * kHeadDim * 2),
+      span("lse_out", a.lse_out, rows * 4),
+      span("mask_out", a.mask_out, mask_bytes),
+      span("stats_out", a.stats_out, (size_t)a.B * (size_t)a.H * 4 * sizeof(uint64_t)),
+  };
+  for (const Span& w : out) {
+    for (const Span& r : in)
+      if (overlap(w, r)) return fail(DSATTN_EINVAL, "%s must not overlap %s", w.name, r.name);
+    for (const Span& w2 : out)
+      if (&w2 < &w && overlap(w, w2))
+        return fail(DSATTN_EINVAL, "%s must not overlap %s", w.name, w2.name);
+  }
+  return DSATTN_OK;
+}
+
 // Pointer checks of a non-empty problem.
 int check_pointers(const dsattn_args& a) {
   if (a.q == nullptr || a.k == nullptr || a.v == nullptr || a.o == nullptr)
@@ -116,8 +163,6 @@ int check_pointers(const dsattn_args& a) {
     if (!aligned(ptrs[i], 16))
       return fail(DSATTN_EINVAL, "%s must be 16-byte aligned", names[i]);
   }
-  if (a.o == a.q || a.o == a.k || a.o == a.v)
-    return fail(DSATTN_EINVAL, "o must not alias q, k or v");
   if (a.stats_out != nullptr && !is_device_pointer(a.stats_out))
     return fail(DSATTN_EINVAL, "stats_out is not a device pointer");
   if (a.mask_out != nullptr && !is_device_pointer(a.mask_out))
@@ -137,9 +182,8 @@ int check_pointers(const dsattn_args& a) {
   if (a.rule == DSATTN_RULE_MASK) {
     if (a.mask_in == nullptr) return fail(DSATTN_EINVAL, "mask reuse needs mask_in");
     if (!is_device_pointer(a.mask_in)) return fail(DSATTN_EINVAL, "mask_in is not a device pointer");
-    if (a.mask_out == a.mask_in) return fail(DSATTN_EINVAL, "mask_out must not alias mask_in");
   }
-  return DSATTN_OK;
+  return check_overlaps(a);
 }
 
 // Zero stats_out of an empty problem (the only output it has).
