@@ -26,8 +26,8 @@
  * Shapes: d must be 128; tile_q is 128 or 32 and tile_k 32, 64 or 128.  tile_k is the
  *   key tile B_c, the number of keys one skip decision covers (Section 4.2.1 uses 128 for
  *   the 14B model and 32 for the 5B model).  The kernels work on 64-key tiles: 128 is two
- *   of them deciding together, 32 their two halves deciding in turn; both visit keys in
- *   ascending order only; tile_q is the number of query rows that share one skip
+ *   of them deciding together, 32 their two halves deciding in turn (ascending order
+ *   only); tile_q is the number of query rows that share one skip
  *   decision ("query tile" below): 128 decides per workgroup tile, 32 lets every 32-row
  *   slice decide on its own (a finer granularity of the same rule, which the paper
  *   leaves open).  B, H, N >= 0, N <= 8388607 and B*H <= 65535; B == 0, H == 0 or
@@ -155,8 +155,9 @@ typedef struct dsattn_args {
  * DSATTN_ORDER_DIAGONAL every 128-row query block starts at the key tile c that holds its
  * first row (c = 128 i / tile_k for block i), then visits c+1, c-1, c+2, c-2, ... and,
  * once one side is used up, the rest of the other side in order; query tiles of 32 rows
- * use the order of their 128-row block.  For self-attention this visits the keys nearest
- * each query first.  mask_out is indexed by key tile whatever the order.
+ * use the order of their 128-row block.  With tile_k = 128 the order runs over 128-key
+ * tiles (c = i); tile_k = 32 takes ascending order only.  For self-attention this visits
+ * the keys nearest each query first.  mask_out is indexed by key tile whatever the order.
  */
 int dsattn_attn_fwd_ex(const dsattn_args* args);
 

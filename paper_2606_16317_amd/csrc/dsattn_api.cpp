@@ -85,13 +85,10 @@ int check_problem(const dsattn_args& a) {
     return fail(DSATTN_EINVAL, "unknown qk format %d", a.qk_format);
   if (a.qk_format == DSATTN_QK_MXFP8 && a.rule == DSATTN_RULE_MASK)
     return fail(DSATTN_EUNSUPPORTED, "mask reuse takes bf16 q and k");
-  if (a.tile_k != kTileK) {
-    if (a.key_order != DSATTN_ORDER_ASCENDING)
-      return fail(DSATTN_EUNSUPPORTED, "tile_k = %d visits key tiles in ascending order only",
-                  a.tile_k);
-    if (a.rule == DSATTN_RULE_MASK && a.tile_k != kTileKPair)
-      return fail(DSATTN_EUNSUPPORTED, "mask reuse takes tile_k = 64 or 128");
-  }
+  if (a.tile_k == kTileKHalf && a.key_order != DSATTN_ORDER_ASCENDING)
+    return fail(DSATTN_EUNSUPPORTED, "tile_k = 32 visits key tiles in ascending order only");
+  if (a.rule == DSATTN_RULE_MASK && a.tile_k == kTileKHalf)
+    return fail(DSATTN_EUNSUPPORTED, "mask reuse takes tile_k = 64 or 128");
   if (a.rule == DSATTN_RULE_MASK) {
     if (a.key_order != DSATTN_ORDER_ASCENDING)
       return fail(DSATTN_EUNSUPPORTED, "mask reuse visits key tiles in ascending order only");

@@ -705,6 +705,22 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
 // requested when the current pair is kept, and a kept pair after a skipped one fetches its
 // first V tile late.
 
+// 64-key tile of loop step j with 128-key decisions: tile j in ascending order; in
+// diagonal-first order pair key_tile_at(j / 2) (the order runs over 128-key tiles, centred
+// on the workgroup's own) and its tile j % 2.  A partial last pair still takes two steps:
+// its second tile lies past the sequence end, so every key of it is masked.  Steps past
+// the loop name a tile past the end.
+template <int ORDER>
+__device__ __forceinline__ int pair_tile(int j, const LoopCtx& cx) {
+  if constexpr (ORDER == kOrderAscending) {
+    return j;
+  } else {
+    const int n_pairs = (cx.n_kt + 1) >> 1;
+    if ((j >> 1) >= n_pairs) return 2 * n_pairs;
+    return 2 * key_tile_at<ORDER>(j >> 1, cx) + (j & 1);
+  }
+}
+
 // Softmax of S_j (lazy reference max already updated) and O += P_j V_j: the first eight
 // elements up front, then two under each of the first twelve P.V MFMAs, so that P block s
 // is complete before MFMA 4 s reads it.
@@ -738,7 +754,7 @@ __device__ __forceinline__ void softmax_pv_tile(RowState& rs, f32x16 (&o)[4],
 // First step of pair m = j / 2.  On entry s_cur holds S_j and mhat its row max; v_ready
 // tells whether V_j was requested in the previous step.  On exit s_next holds S_{j+1},
 // mhat the pair's row max, keep_own / keep_any the pair's decisions.
-template <int RULE, int UNIT, bool Q8>
+template <int RULE, int UNIT, bool Q8, int ORDER>
 __device__ __forceinline__ void pair_first_step(int j, const f32x16 (&s_cur)[2],
                                                 f32x16 (&s_next)[2], float& mhat,
                                                 bool& keep_own, bool& keep_any, bool& v_ready,
@@ -746,14 +762,15 @@ __device__ __forceinline__ void pair_first_step(int j, const f32x16 (&s_cur)[2],
                                                 const typename QFragOf<Q8>::type& qf,
                                                 Smem& sm, const LoopCtx& cx, SkipCount& sk) {
   const int nb = (j + 1) & 1;
-  load_k_tile<Q8>(sm, j & 1, cx, (j + 2) * kTK);
+  const int tj = pair_tile<ORDER>(j, cx);             // the pair's two tiles: tj, tj + 1
+  load_k_tile<Q8>(sm, j & 1, cx, pair_tile<ORDER>(j + 2, cx) * kTK);
   if constexpr (Q8)
     skipped_tile_q8(s_next, reinterpret_cast<const uint8_t*>(sm.k[nb]), sm.ks[nb], qf, cx.r,
                     cx.g);
   else
     skipped_tile(s_next, sm.k[nb], qf, cx.r, cx.g);
   // Keys past the end (a partial last tile, or no second tile at all) do not count.
-  if ((j + 2) * kTK > cx.N) mask_tail(s_next, (j + 1) * kTK, cx.N, cx.g);
+  if ((tj + 2) * kTK > cx.N) mask_tail(s_next, (tj + 1) * kTK, cx.N, cx.g);
   const float mhat_pair = fmaxf(mhat, row_max(s_next) * cx.c);
   if constexpr (RULE != kRuleDense) {
     const bool wave_keeps = __ballot(cx.valid & row_keeps<RULE>(rs, mhat_pair, cx.thr)) != 0;
@@ -763,18 +780,18 @@ __device__ __forceinline__ void pair_first_step(int j, const f32x16 (&s_cur)[2],
     keep_own = UNIT == kTQ ? keep_any : wave_keeps;
   }
   if (cx.mask_row != nullptr && (UNIT == kTQ ? cx.w == 0 : true) && cx.lane == 0)
-    cx.mask_row[j >> 1] = keep_own ? 0 : 1;
+    cx.mask_row[tj >> 1] = keep_own ? 0 : 1;
   if (keep_any && !v_ready) {
-    load_tile_lds(sm.v[j & 1], cx.vrs, cx.voff, j * kTK, cx.w);
+    load_tile_lds(sm.v[j & 1], cx.vrs, cx.voff, tj * kTK, cx.w);
     asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
   }
-  if (keep_any) load_tile_lds(sm.v[nb], cx.vrs, cx.voff, (j + 1) * kTK, cx.w);
+  if (keep_any) load_tile_lds(sm.v[nb], cx.vrs, cx.voff, (tj + 1) * kTK, cx.w);
   if (keep_own) {
     rescale_if_needed(rs, o, mhat_pair);
     softmax_pv_tile(rs, o, s_cur, cx.c, sm.v[j & 1], cx.lane);
   } else {
     sk.tiles += 1;
-    sk.elems += (uint64_t)cx.rows_valid * (uint64_t)min(2 * kTK, cx.N - j * kTK);
+    sk.elems += (uint64_t)cx.rows_valid * (uint64_t)min(2 * kTK, cx.N - tj * kTK);
   }
   v_ready = keep_any;
   mhat = mhat_pair;
@@ -783,7 +800,7 @@ __device__ __forceinline__ void pair_first_step(int j, const f32x16 (&s_cur)[2],
 
 // Second step of the pair (tile j = 2m + 1, decisions from the first step): the tile
 // body, which also computes S_{j+1} of the next pair's first tile.
-template <int RULE, int UNIT, bool Q8>
+template <int RULE, int UNIT, bool Q8, int ORDER>
 __device__ __forceinline__ void pair_second_step(int j, const f32x16 (&s_cur)[2],
                                                  f32x16 (&s_next)[2], float& mhat,
                                                  bool keep_own, bool keep_any, bool& v_ready,
@@ -791,8 +808,9 @@ __device__ __forceinline__ void pair_second_step(int j, const f32x16 (&s_cur)[2]
                                                  const typename QFragOf<Q8>::type& qf,
                                                  Smem& sm, const LoopCtx& cx) {
   const int nb = (j + 1) & 1;
-  load_k_tile<Q8>(sm, j & 1, cx, (j + 2) * kTK);
-  if (keep_any) load_tile_lds(sm.v[nb], cx.vrs, cx.voff, (j + 1) * kTK, cx.w);
+  const int tn = pair_tile<ORDER>(j + 1, cx);        // the next pair's first tile
+  load_k_tile<Q8>(sm, j & 1, cx, pair_tile<ORDER>(j + 2, cx) * kTK);
+  if (keep_any) load_tile_lds(sm.v[nb], cx.vrs, cx.voff, tn * kTK, cx.w);
   if (keep_own) {
     if constexpr (Q8)
       kept_tile_q8(rs, o, s_cur, mhat, cx.c, s_next, reinterpret_cast<const uint8_t*>(sm.k[nb]),
@@ -808,8 +826,8 @@ __device__ __forceinline__ void pair_second_step(int j, const f32x16 (&s_cur)[2]
       skipped_tile(s_next, sm.k[nb], qf, cx.r, cx.g);
   }
   v_ready = keep_any;
-  if (j + 1 < cx.n_kt) {
-    if ((j + 2) * kTK > cx.N) mask_tail(s_next, (j + 1) * kTK, cx.N, cx.g);
+  if (tn < cx.n_kt) {
+    if ((tn + 1) * kTK > cx.N) mask_tail(s_next, tn * kTK, cx.N, cx.g);
     mhat = row_max(s_next) * cx.c;
   }
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
@@ -1070,8 +1088,8 @@ __device__ __forceinline__ void half_tile_step(int j, const f32x16 (&s_cur)[2],
 // ORDER: key-tile visit order (ascending or diagonal-first).
 // Q8: Q and K in MX-FP8 (codes p.q8 / p.k8, exponents p.q_scales / p.k_scales), S = Q K^T
 // on the scaled fp8 MFMA; everything after S is the same as with bf16 Q and K.
-// BC: keys per skip decision: 64 (one tile), 128 (two tiles) or 32 (half a tile); 128
-// and 32 walk keys in ascending order only.
+// BC: keys per skip decision: 64 (one tile), 128 (two tiles) or 32 (half a tile); 32
+// walks keys in ascending order only.
 template <int RULE, int UNIT, int ORDER, bool Q8, int BC = kTK>
 __global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads),
                           amdgpu_waves_per_eu(2, 2))) void
@@ -1133,12 +1151,15 @@ fa_fwd_kernel(FwdParams p) {
   cx.mask_row = (p.mask != nullptr && cx.rows_valid > 0)
                     ? p.mask + ((size_t)bh * p.n_qu + unit) * (BC == kTK ? p.n_kt : p.n_kd)
                     : nullptr;
-  cx.diag_c = q0 / kTK;                               // < n_kt since q0 < N
-  cx.diag_m = min(cx.diag_c, cx.n_kt - 1 - cx.diag_c);
-  cx.diag_right = (cx.n_kt - 1 - cx.diag_c) > cx.diag_c;
+  // Diagonal-first order starts at the key tile holding the first query row: over 64-key
+  // tiles, or over 128-key tiles with 128-key decisions.
+  const int n_order = PAIR ? (cx.n_kt + 1) / 2 : cx.n_kt;
+  cx.diag_c = PAIR ? q0 / (2 * kTK) : q0 / kTK;       // < n_order since q0 < N
+  cx.diag_m = min(cx.diag_c, n_order - 1 - cx.diag_c);
+  cx.diag_right = (n_order - 1 - cx.diag_c) > cx.diag_c;
 
   // Stage K and V of the first visited tile, then K of the second.
-  const int t0 = key_tile_at<ORDER>(0, cx);
+  const int t0 = PAIR ? pair_tile<ORDER>(0, cx) : key_tile_at<ORDER>(0, cx);
   load_k_tile<Q8>(sm, 0, cx, t0 * kTK);
   load_tile_lds(sm.v[0], cx.vrs, cx.voff, t0 * kTK, cx.w);
 
@@ -1177,7 +1198,7 @@ fa_fwd_kernel(FwdParams p) {
   for (int db = 0; db < 4; ++db) o[db] = f32x16{};
   RowState rs{-__builtin_inff(), -__builtin_inff(), 0.f};
 
-  load_k_tile<Q8>(sm, 1, cx, key_tile_or_past<ORDER>(1, cx) * kTK);
+  load_k_tile<Q8>(sm, 1, cx, (PAIR ? pair_tile<ORDER>(1, cx) : key_tile_or_past<ORDER>(1, cx)) * kTK);
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 
   f32x16 sa[2], sb[2];
@@ -1207,13 +1228,15 @@ fa_fwd_kernel(FwdParams p) {
                                        cx, sk);
     }
   } else if constexpr (PAIR) {
-    static_assert(ORDER == kOrderAscending, "128-key decisions walk keys in ascending order");
-    for (int j = 0; j < cx.n_kt; j += 2) {
-      pair_first_step<RULE, UNIT, Q8>(j, sa, sb, mhat, keep_own, keep_any, v_ready, rs, o, qf,
-                                      sm, cx, sk);
-      if (j + 1 < cx.n_kt)
-        pair_second_step<RULE, UNIT, Q8>(j + 1, sb, sa, mhat, keep_own, keep_any, v_ready, rs,
-                                         o, qf, sm, cx);
+    // Ascending: the last pair is the partial one and may end after one step.  Diagonal:
+    // every pair takes two steps (a partial pair's second tile is all masked).
+    const int n_steps = ORDER == kOrderAscending ? cx.n_kt : 2 * ((cx.n_kt + 1) / 2);
+    for (int j = 0; j < n_steps; j += 2) {
+      pair_first_step<RULE, UNIT, Q8, ORDER>(j, sa, sb, mhat, keep_own, keep_any, v_ready, rs,
+                                             o, qf, sm, cx, sk);
+      if (j + 1 < n_steps)
+        pair_second_step<RULE, UNIT, Q8, ORDER>(j + 1, sb, sa, mhat, keep_own, keep_any,
+                                                v_ready, rs, o, qf, sm, cx);
     }
   } else {
     // Unrolled by two so that S_j / S_{j+1} alternate between sa and sb without copies.
@@ -1479,7 +1502,7 @@ hipError_t launch_unit(int rule, const FwdParams& p, dim3 grid, hipStream_t stre
   return hipGetLastError();
 }
 
-template <int UNIT, bool Q8>
+template <int UNIT, bool Q8, int ORDER>
 hipError_t launch_pair(int rule, const FwdParams& p, dim3 grid, hipStream_t stream) {
   const dim3 block(kThreads);
   switch (rule) {
@@ -1488,12 +1511,12 @@ hipError_t launch_pair(int rule, const FwdParams& p, dim3 grid, hipStream_t stre
                          block, 0, stream, p);
       break;
     case kRuleBlasst:
-      hipLaunchKernelGGL((fa_fwd_kernel<kRuleBlasst, UNIT, kOrderAscending, Q8, 2 * kTK>), grid,
-                         block, 0, stream, p);
+      hipLaunchKernelGGL((fa_fwd_kernel<kRuleBlasst, UNIT, ORDER, Q8, 2 * kTK>), grid, block, 0,
+                         stream, p);
       break;
     case kRuleDynSparse:
-      hipLaunchKernelGGL((fa_fwd_kernel<kRuleDynSparse, UNIT, kOrderAscending, Q8, 2 * kTK>), grid,
-                         block, 0, stream, p);
+      hipLaunchKernelGGL((fa_fwd_kernel<kRuleDynSparse, UNIT, ORDER, Q8, 2 * kTK>), grid, block,
+                         0, stream, p);
       break;
     default:
       return hipErrorInvalidValue;
@@ -1526,8 +1549,13 @@ hipError_t launch_half(int rule, const FwdParams& p, dim3 grid, hipStream_t stre
 template <int UNIT, bool Q8>
 hipError_t launch_order(int rule, const FwdParams& p, dim3 grid, hipStream_t stream) {
   if (p.key_tile == 2 * kTK) {
-    if (p.key_order != kOrderAscending) return hipErrorInvalidValue;
-    return launch_pair<UNIT, Q8>(rule, p, grid, stream);
+    if (p.key_order == kOrderDiagonal && rule != kRuleDense) {
+      const int chunk = (p.n_qt + kXcds - 1) / kXcds;
+      return launch_pair<UNIT, Q8, kOrderDiagonal>(rule, p,
+                                                   dim3((unsigned)(chunk * kXcds), grid.y),
+                                                   stream);
+    }
+    return launch_pair<UNIT, Q8, kOrderAscending>(rule, p, grid, stream);
   }
   if (p.key_tile == kTK / 2) {
     if (p.key_order != kOrderAscending) return hipErrorInvalidValue;

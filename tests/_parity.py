@@ -42,7 +42,7 @@ class GpuRun:
 
 
 def run_gpu(qd, kd, vd, rule: str, param: float, scale: float, tile_q: int = TILE_Q,
-            tile_k: int = TILE_K) -> GpuRun:
+            tile_k: int = TILE_K, key_order: int = 0) -> GpuRun:
     import torch
     import paper_2606_16317_amd as dsa
 
@@ -53,7 +53,8 @@ def run_gpu(qd, kd, vd, rule: str, param: float, scale: float, tile_q: int = TIL
     mask = torch.full((B * H * n_qt * n_kt,), 7, dtype=torch.uint8, device=qd.device)
     lse = torch.full((B * H * N,), float("nan"), dtype=torch.float32, device=qd.device)
     dsa.dsattn_attn_fwd_ex(RULE_NAMES[rule], param, qd, kd, vd, o, scale=scale, tile_q=tile_q,
-                           tile_k=tile_k, stats_out=stats, mask_out=mask, lse_out=lse)
+                           tile_k=tile_k, stats_out=stats, mask_out=mask, lse_out=lse,
+                           key_order=key_order)
     torch.cuda.synchronize()
     return GpuRun(from_device_bf16(o), mask.cpu().numpy().reshape(B, H, n_qt, n_kt),
                   lse.cpu().numpy().reshape(B, H, N), stats.cpu().numpy().reshape(B, H, 4))

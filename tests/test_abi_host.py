@@ -343,14 +343,14 @@ def test_key_mean_and_shifted_quantize_host_checks():
     assert rc == 0 and err == ""
 
 
-def test_key_tile_128_restrictions():
+def test_key_tile_restrictions():
     pkg = _lib()
     L = pkg.lib()
     a = pkg.DsAttnArgs(pkg.RULE_DYNSPARSE_LAMBDA, -6.0, None, None, None, None, 1, 1, 256,
                        128, 0.1, 128, 128, None, None, None, None, pkg.ORDER_DIAGONAL, None, 0,
                        None, None)
-    assert L.dsattn_attn_fwd_ex(ctypes.byref(a)) == -2
-    assert "ascending" in pkg.last_error()
+    assert L.dsattn_attn_fwd_ex(ctypes.byref(a)) == -1      # 128 in diagonal order: supported
+    assert "non-null" in pkg.last_error()
     a.key_order, a.rule = pkg.ORDER_ASCENDING, pkg.RULE_MASK
     assert L.dsattn_attn_fwd_ex(ctypes.byref(a)) == -1      # 128-key masks are reusable
     assert "mask_in" in pkg.last_error() or "non-null" in pkg.last_error()

@@ -127,6 +127,42 @@ def test_concentrated_heads_skip(peaked, tk, tile_q, rule, param):
             assert recall.min() >= param - 2e-3
 
 
+@pytest.mark.parametrize("tile_q", [128, 32])
+@pytest.mark.parametrize("rule,param", [("dynsparse_lambda", -6.0), ("dynsparse_recall", 0.9),
+                                        ("blasst", 1e-2)])
+def test_128_key_decisions_in_diagonal_order(peaked, tile_q, rule, param):
+    """Diagonal-first order over 128-key tiles: each 128-row block starts at its own
+    128-key tile; the oracle runs the same order (``key_order="diagonal"``)."""
+    (q, k, v), dev = peaked
+    announce(f"tile_k=128 diagonal peaked tile_q={tile_q} rule={rule} param={param}")
+    g = run_gpu(*dev, rule, param, SCALE, tile_q=tile_q, tile_k=TK, key_order=1)
+    rep = compare(q, k, v, g, rule, param, SCALE, tile_q=tile_q, tile_k=TK,
+                  key_order="diagonal")
+    print(rep, flush=True)
+    assert_parity(rep)
+    assert rep.sparsity > 0.1
+    N = q.shape[2]
+    assert (g.stats == expected_stats_from_mask(g.mask, N, tile_q, TK)).all()
+    for i in range(g.mask.shape[2]):                 # each block's own tile is kept
+        assert not g.mask[..., i, (i * tile_q) // 128].any()
+
+
+@pytest.mark.parametrize("N", [65, 191, 700, 1000, 1601])
+def test_128_key_diagonal_ragged(N):
+    """Ragged sequences: a partial last 128-key tile (one or one and a half 64-key tiles)
+    that the diagonal order visits in the middle of the walk for some query tiles."""
+    q, k, v = make_random_qkv(1, 2, N, 128, 6100 + N, q_std=1.5, k_std=1.5)
+    dev = upload(q, k, v)
+    for tile_q in (128, 32):
+        announce(f"tile_k=128 diagonal ragged N={N} tile_q={tile_q}")
+        g = run_gpu(*dev, "dynsparse_lambda", -3.0, SCALE, tile_q=tile_q, tile_k=TK,
+                    key_order=1)
+        assert_parity(compare(q, k, v, g, "dynsparse_lambda", -3.0, SCALE, tile_q=tile_q,
+                              tile_k=TK, key_order="diagonal"))
+        assert (g.stats == expected_stats_from_mask(g.mask, N, tile_q, TK)).all()
+        assert not np.isnan(g.lse).any()
+
+
 @pytest.mark.parametrize("tk", KEY_TILES)
 def test_infinite_threshold_equals_dense(peaked, tk):
     """At recall 1 (lambda = -inf) and tau = 0 the rule kernels keep everything and
