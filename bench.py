@@ -351,7 +351,7 @@ def sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop):
     B, H, N = w.B, w.H, w.N
     # 128-row decisions in ascending key order (the default); then every wave's 32 rows
     # deciding on their own (tile_q = 32); then the diagonal-first key order.
-    # 128- and 32-key decisions (tile_k = 128, 32) close the list.
+    # 128-key decisions (tile_k = 128, both orders) and 32-key decisions close the list.
     asc, diag = dsa.ORDER_ASCENDING, dsa.ORDER_DIAGONAL
     points = [("dense", 0.0, TILE_Q, asc)] + \
              [("dynsparse_recall", r, TILE_Q, asc) for r in (0.90, 0.95, 0.98, 0.99)] + \
@@ -369,6 +369,9 @@ def sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop):
               ("dynsparse_lambda", -8.0, TILE_Q, asc, 128),
               ("dynsparse_lambda", -10.0, TILE_Q, asc, 128), ("blasst", 1e-2, TILE_Q, asc, 128),
               ("dynsparse_lambda", -6.0, 32, asc, 128),
+              ("dynsparse_recall", 0.95, TILE_Q, diag, 128),
+              ("dynsparse_lambda", -6.0, TILE_Q, diag, 128),
+              ("dynsparse_lambda", -8.0, TILE_Q, diag, 128),
               ("dense", 0.0, TILE_Q, asc, 32), ("dynsparse_recall", 0.95, TILE_Q, asc, 32),
               ("dynsparse_lambda", -6.0, TILE_Q, asc, 32),
               ("dynsparse_lambda", -8.0, TILE_Q, asc, 32),
