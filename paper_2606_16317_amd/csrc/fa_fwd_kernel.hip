@@ -71,6 +71,7 @@ constexpr int kTQ = 128;       // query rows per workgroup (decision granularity
 constexpr int kTK = 64;        // keys per tile
 constexpr int kXcds = 8;       // accelerator dies; workgroups are dealt to them round-robin
 constexpr int kWaves = 4;
+constexpr uint32_t kAllSkip = 0x01010101u;  // skip word in which every wave votes skip
 constexpr int kThreads = kWaves * 64;
 constexpr int kTileElems = kTK * kD;         // 8192 bf16 = 16 KiB
 constexpr float kRescaleSlack = 8.0f;        // log2 units
@@ -601,14 +602,19 @@ __device__ __forceinline__ void load_k_tile(Smem& sm, int buf, const LoopCtx& cx
 
 // One loop step j, visiting key tile key_tile_at(j) (written "tile j" below; LDS buffers
 // rotate with the step).  On entry s_cur holds S_j, mhat its row max (log2 units), vote the
-// workgroup's vote word for tile j (one byte per wave, loaded after the last barrier and
-// read only once the next K tile's DMA is out, so that the LDS latency overlaps it),
-// keep_own the decision for tile j of this wave's decision unit when that unit is the
-// wave's own 32 rows (UNIT = 32; with the workgroup's 128 rows it comes from the vote),
-// and v_ready whether V_j is already in LDS (buffer j % 2).  keep_any (some unit of the
-// workgroup keeps tile j) is set from the vote.  On exit s_next holds
-// S_{j+1}, the other state refers to tile j+1, and every wave has passed the barrier that
-// publishes K_{j+2}, the V_{j+1} buffer if it was requested, and the tile-(j+1) votes.
+// workgroup's skip word for tile j as this wave needs it (below), keep_own the decision for
+// tile j of this wave's decision unit when that unit is the wave's own 32 rows (UNIT = 32;
+// with the workgroup's 128 rows it comes from the vote), and v_ready whether V_j is already
+// in LDS (buffer j % 2).  keep_any (some unit of the workgroup keeps tile j) is set from
+// the vote.  On exit s_next holds S_{j+1}, the other state refers to tile j+1, and every
+// wave has passed the barrier that publishes K_{j+2}, the V_{j+1} buffer if it was
+// requested, and the tile-(j+1) votes.
+//
+// Votes.  Byte w of vote buffer b is 1 while wave w's last vote in that buffer was "skip".
+// A wave writes its byte only when its vote changes (marks records which of its two bytes
+// are set), and only a wave that votes skip reads the word back: one that keeps the tile
+// knows that the workgroup keeps it.  The workgroup skips a tile when all four bytes are 1.
+// With nothing skipped the votes therefore cost no LDS traffic at all.
 //
 // V tiles are fetched for tiles some unit keeps.  V_{j+1} is requested one iteration
 // ahead when tile j is kept (runs of kept tiles are the common case); after a skipped
@@ -617,8 +623,8 @@ __device__ __forceinline__ void load_k_tile(Smem& sm, int buf, const LoopCtx& cx
 template <int RULE, int UNIT, int ORDER, bool Q8>
 __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f32x16 (&s_next)[2],
                                               float& mhat, bool& keep_own, bool& keep_any,
-                                              uint32_t& vote, bool& v_ready, RowState& rs,
-                                              f32x16 (&o)[4],
+                                              uint32_t& vote, uint32_t& marks, bool& v_ready,
+                                              RowState& rs, f32x16 (&o)[4],
                                               const typename QFragOf<Q8>::type& qf, Smem& sm,
                                               const LoopCtx& cx, SkipCount& sk) {
   const int nb = (j + 1) & 1;
@@ -626,11 +632,11 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
   const int tj = key_tile_at<ORDER>(j, cx);          // key tiles of steps j, j+1, j+2
   const int tn = key_tile_or_past<ORDER>(j + 1, cx);
   const int tn2 = key_tile_or_past<ORDER>(j + 2, cx);
-  // The K tile two steps ahead does not depend on the decision: its DMA goes out while the
+  // The K tile two steps ahead does not depend on the decision: its DMA goes out while a
   // vote word read after the last barrier is still in flight.
   load_k_tile<Q8>(sm, j & 1, cx, tn2 * kTK);
   if constexpr (RULE != kRuleDense) {
-    keep_any = __builtin_amdgcn_readfirstlane(vote) != 0;
+    keep_any = __builtin_amdgcn_readfirstlane(vote) != kAllSkip;
     if constexpr (UNIT == kTQ) keep_own = keep_any;
   }
   if (cx.mask_row != nullptr && (UNIT == kTQ ? cx.w == 0 : true) && cx.lane == 0)
@@ -675,7 +681,11 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
     mhat_next = row_max(s_next) * cx.c;
     if constexpr (RULE != kRuleDense) {
       wave_keeps = __ballot(cx.valid & row_keeps<RULE>(rs, mhat_next, cx.thr)) != 0;
-      if (cx.lane == 0) sm.vote[nb][cx.w] = wave_keeps ? 1 : 0;
+      const uint32_t mark = wave_keeps ? 0u : 1u;
+      if (mark != ((marks >> nb) & 1u)) {
+        if (cx.lane == 0) sm.vote[nb][cx.w] = (uint8_t)mark;
+        marks ^= 1u << nb;
+      }
     }
   }
   // Publish this wave's LDS traffic and its tile loads (read in the next iteration), then
@@ -684,7 +694,12 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
   if (has_next) {
     if constexpr (RULE != kRuleDense) {
-      vote = *reinterpret_cast<const uint32_t*>(sm.vote[nb]);   // consumed by the next step
+      // Consumed by the next step.  The atomic load keeps the read under the branch.
+      if (wave_keeps)
+        vote = 0u;
+      else
+        vote = __atomic_load_n(reinterpret_cast<const uint32_t*>(sm.vote[nb]),
+                               __ATOMIC_RELAXED);
       if constexpr (UNIT != kTQ) keep_own = wave_keeps;
     }
     mhat = mhat_next;
@@ -1199,6 +1214,10 @@ fa_fwd_kernel(FwdParams p) {
   RowState rs{-__builtin_inff(), -__builtin_inff(), 0.f};
 
   load_k_tile<Q8>(sm, 1, cx, (PAIR ? pair_tile<ORDER>(1, cx) : key_tile_or_past<ORDER>(1, cx)) * kTK);
+  if (cx.lane == 0) {                        // vote bytes start at 0 (not skipping)
+    sm.vote[0][cx.w] = 0;
+    sm.vote[1][cx.w] = 0;
+  }
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 
   f32x16 sa[2], sb[2];
@@ -1210,7 +1229,8 @@ fa_fwd_kernel(FwdParams p) {
   float mhat = row_max(sa) * cx.c;
   bool keep_own = true;                      // the first tile is always kept
   bool keep_any = true;
-  uint32_t vote = 1;                         // the first tile's "vote": kept
+  uint32_t vote = 0;                         // the first tile's skip word: kept
+  uint32_t marks = 0;                        // this wave's vote bytes that hold 1
   bool v_ready = true;                       // V_0 was staged above
   SkipCount sk;
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");  // K_0 consumed
@@ -1241,11 +1261,11 @@ fa_fwd_kernel(FwdParams p) {
   } else {
     // Unrolled by two so that S_j / S_{j+1} alternate between sa and sb without copies.
     for (int j = 0; j < cx.n_kt; j += 2) {
-      key_tile_step<RULE, UNIT, ORDER, Q8>(j, sa, sb, mhat, keep_own, keep_any, vote, v_ready,
-                                           rs, o, qf, sm, cx, sk);
+      key_tile_step<RULE, UNIT, ORDER, Q8>(j, sa, sb, mhat, keep_own, keep_any, vote, marks,
+                                           v_ready, rs, o, qf, sm, cx, sk);
       if (j + 1 < cx.n_kt)
         key_tile_step<RULE, UNIT, ORDER, Q8>(j + 1, sb, sa, mhat, keep_own, keep_any, vote,
-                                             v_ready, rs, o, qf, sm, cx, sk);
+                                             marks, v_ready, rs, o, qf, sm, cx, sk);
     }
   }
 
