@@ -14,6 +14,7 @@ from .video_qkv import (
     make_video_qkv,
     workload_inputs,
 )
+from .vote_patterns import expected_skip, vote_pattern_inputs
 
 __all__ = [
     "WORKLOADS",
@@ -23,4 +24,6 @@ __all__ = [
     "make_random_qkv",
     "make_video_qkv",
     "workload_inputs",
+    "vote_pattern_inputs",
+    "expected_skip",
 ]
