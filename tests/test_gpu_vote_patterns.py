@@ -75,3 +75,26 @@ def test_mask_matches_closed_form_mxfp8(tile_q):
     torch.cuda.synchronize()
     got = mask.cpu().numpy().reshape(1, 2, n_units, -1)
     assert np.array_equal(got, expected_skip(pattern, N, tile_q))
+
+
+@pytest.mark.parametrize("tile_k,key_order", [(32, 0), (128, 0), (64, 1), (128, 1)])
+@pytest.mark.parametrize("tile_q", [128, 32])
+@pytest.mark.parametrize("rule,param", [("dynsparse_lambda", -10.0), ("blasst", 1e-4)])
+def test_mask_closed_form_key_tiles(tile_k, key_order, tile_q, rule, param):
+    """32-key pattern tiles: 32-key decisions (two halves of each 64-key tile, the second
+    voted after the first), 128-key pair decisions and diagonal-first order all give the
+    closed-form mask."""
+    N = 2348
+    q, k, v, pattern = vote_pattern_inputs(N, 2, seed=58, p_bit=0.12, pattern_tile=32)
+    order = "diagonal" if key_order else "ascending"
+    announce(f"vote patterns N={N} tile_q={tile_q} tile_k={tile_k} order={order} rule={rule}")
+    g = run_gpu(to_device(q), to_device(k), to_device(v), rule, param, SCALE, tile_q=tile_q,
+                tile_k=tile_k, key_order=key_order)
+    assert np.array_equal(g.mask, expected_skip(pattern, N, tile_q, tile_k=tile_k,
+                                                pattern_tile=32))
+    assert (g.stats == expected_stats_from_mask(g.mask, N, tile_q, tile_k)).all()
+    rep = compare(q, k, v, g, rule, param, SCALE, tile_q=tile_q, tile_k=tile_k,
+                  key_order=order)
+    print(rep, flush=True)
+    assert_parity(rep)
+    assert rep.mismatches == 0

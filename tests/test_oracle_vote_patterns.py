@@ -44,3 +44,22 @@ def test_patterns_cover_every_vote_transition():
     assert flips.any(axis=(0, 1, 2)).all()
     counts = np.unique(bits.sum(axis=-1))
     assert set(counts.tolist()) >= {0, 1, 2, 3, 4}
+
+
+@pytest.mark.parametrize("tile_k,key_order", [(32, "ascending"), (64, "ascending"),
+                                              (128, "ascending"), (64, "diagonal"),
+                                              (128, "diagonal")])
+@pytest.mark.parametrize("unit", [128, 32])
+@pytest.mark.parametrize("rule,thr", [("dynsparse", -10.0), ("blasst", math.log(1e-4))])
+def test_oracle_mask_closed_form_key_tiles(tile_k, key_order, unit, rule, thr):
+    """32-key pattern tiles: B_c = 32 decides each pattern tile, 64 and 128 the OR of two
+    and four; the same mask in ascending and diagonal-first order."""
+    N = 2348
+    q, k, v, pattern = vote_pattern_inputs(N, 1, seed=43, p_bit=0.12, pattern_tile=32)
+    run = oracle.rule_attention(q, k, v, SCALE, rule, thr, unit, tile_k, key_order=key_order)
+    want = expected_skip(pattern, N, unit, tile_k=tile_k, pattern_tile=32)
+    got = np.stack([r.skip for r in run.results]).astype(np.uint8)
+    assert np.array_equal(got, want[0, 0])
+    margins = np.concatenate([np.delete(r.margin, np.argmax(r.margin)) for r in run.results])
+    assert np.abs(margins).min() > 3.0
+    assert 0.05 < want.mean() < 0.95
