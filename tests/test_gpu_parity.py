@@ -252,3 +252,27 @@ def test_wan720p_sweep_sampled():
 def test_stress_sampled():
     _full("stress", [("dynsparse_recall", 0.95), ("dynsparse_lambda", -6.0)], n_heads=4,
           seed=4)
+
+
+@pytest.mark.slow
+def test_long_sequence_sampled():
+    """One head of N = 2^20 + 37 keys (a 256 MiB K and V slab each, ragged last tiles):
+    in-head byte offsets far beyond the video layers', sampled query tiles including the
+    first and the last, under a threshold that skips most tiles and under dense."""
+    N = (1 << 20) + 37
+    announce(f"generate random head N={N}")
+    q, k, v = make_random_qkv(1, 1, N, 128, 77, q_std=1.5, k_std=1.5)
+    dev = upload(q, k, v)
+    n_qt = -(-N // 128)
+    every = [(0, 0, 0), (0, 0, 4097), (0, 0, n_qt - 1)]
+    for rule, param, tiles in [("dynsparse_lambda", -8.0, every),
+                               ("dense", 0.0, every[-1:])]:
+        announce(f"long sequence rule={rule} param={param}")
+        g = run_gpu(*dev, rule, param, SCALE)
+        rep = compare(q, k, v, g, rule, param, SCALE, tiles=tiles)
+        print(rep, f"full-run tile sparsity={float(g.mask.mean()):.4f}", flush=True)
+        assert_parity(rep)
+        assert (g.stats == expected_stats_from_mask(g.mask, N)).all()
+        if rule != "dense":
+            assert 0.05 < float(g.mask.mean()) < 0.999
+    del dev
