@@ -34,7 +34,7 @@ RULE_NAMES = {"dense": 0, "blasst": 1, "dynsparse_recall": 2, "dynsparse_lambda"
 
 
 @dataclass
-class GpuRun:
+class DeviceRun:
     o: np.ndarray        # uint16 [B,H,N,d]
     mask: np.ndarray     # uint8 [B,H,n_qt,n_kt]
     lse: np.ndarray      # float32 [B,H,N]
@@ -42,7 +42,7 @@ class GpuRun:
 
 
 def run_gpu(qd, kd, vd, rule: str, param: float, scale: float, tile_q: int = TILE_Q,
-            tile_k: int = TILE_K, key_order: int = 0) -> GpuRun:
+            tile_k: int = TILE_K, key_order: int = 0) -> DeviceRun:
     import torch
     import paper_2606_16317_amd as dsa
 
@@ -56,7 +56,7 @@ def run_gpu(qd, kd, vd, rule: str, param: float, scale: float, tile_q: int = TIL
                            tile_k=tile_k, stats_out=stats, mask_out=mask, lse_out=lse,
                            key_order=key_order)
     torch.cuda.synchronize()
-    return GpuRun(from_device_bf16(o), mask.cpu().numpy().reshape(B, H, n_qt, n_kt),
+    return DeviceRun(from_device_bf16(o), mask.cpu().numpy().reshape(B, H, n_qt, n_kt),
                   lse.cpu().numpy().reshape(B, H, N), stats.cpu().numpy().reshape(B, H, 4))
 
 
@@ -100,7 +100,7 @@ class Report:
     lse_max_err: float
 
 
-def compare(q, k, v, g: GpuRun, rule: str, param: float, scale: float, tiles=None,
+def compare(q, k, v, g: DeviceRun, rule: str, param: float, scale: float, tiles=None,
             tile_q: int = TILE_Q, key_order: str = "ascending", tile_k: int = TILE_K) -> Report:
     """Teacher-forced comparison of a GPU run with the oracle over ``tiles`` (b, h, qi),
     where qi counts query tiles of ``tile_q`` rows (the decision unit)."""

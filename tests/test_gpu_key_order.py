@@ -14,7 +14,7 @@ import pytest
 
 from synth import WORKLOADS, make_random_qkv, make_video_qkv, workload_inputs
 
-from _parity import (GpuRun, RULE_NAMES, TILE_K, assert_parity, expected_stats_from_mask,
+from _parity import (DeviceRun, RULE_NAMES, TILE_K, assert_parity, expected_stats_from_mask,
                      from_device_bf16, oracle_rule, sample_tiles, to_device)
 
 import oracle
@@ -53,7 +53,7 @@ def run_diag(qd, kd, vd, rule, param, tile_q=128, key_order=1):
     dsa.dsattn_attn_fwd_ex(RULE_NAMES[rule], param, qd, kd, vd, o, scale=SCALE, tile_q=tile_q,
                            stats_out=stats, mask_out=mask, lse_out=lse, key_order=key_order)
     torch.cuda.synchronize()
-    return GpuRun(from_device_bf16(o), mask.cpu().numpy().reshape(B, H, n_qt, n_kt),
+    return DeviceRun(from_device_bf16(o), mask.cpu().numpy().reshape(B, H, n_qt, n_kt),
                   lse.cpu().numpy().reshape(B, H, N), stats.cpu().numpy().reshape(B, H, 4))
 
 

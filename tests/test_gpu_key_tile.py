@@ -21,7 +21,7 @@ import oracle
 from oracle.mxfp8 import dequantize_mxfp8, quantize_mxfp8
 from synth import make_random_qkv, make_video_qkv, workload_inputs
 
-from _parity import (GpuRun, RULE_NAMES, assert_parity, compare, expected_stats_from_mask,
+from _parity import (DeviceRun, RULE_NAMES, assert_parity, compare, expected_stats_from_mask,
                      from_device_bf16, run_gpu, sample_tiles, to_device)
 
 pytestmark = pytest.mark.gpu
@@ -212,7 +212,7 @@ def test_mxfp8_with_key_tiles(peaked, tk, rule, param):
                               o, scale=SCALE, tile_k=tk, stats_out=stats, mask_out=mask,
                               lse_out=lse)
     torch.cuda.synchronize()
-    g = GpuRun(from_device_bf16(o), mask.cpu().numpy().reshape(B, H, N // 128, n_kd),
+    g = DeviceRun(from_device_bf16(o), mask.cpu().numpy().reshape(B, H, N // 128, n_kd),
                lse.cpu().numpy().reshape(B, H, N), stats.cpu().numpy().reshape(B, H, 4))
     rep = compare(dequantize_mxfp8(qc, qs), dequantize_mxfp8(kc, ks), v, g, rule, param, SCALE,
                   tile_k=tk, tiles=sample_tiles(B, H, N, per_head=4, seed=2))

@@ -17,7 +17,7 @@ import pytest
 import oracle
 from synth import WORKLOADS, make_random_qkv, make_video_qkv, workload_inputs
 
-from _parity import (GpuRun, RULE_NAMES, TILE_K, expected_stats_from_mask, from_device_bf16,
+from _parity import (DeviceRun, RULE_NAMES, TILE_K, expected_stats_from_mask, from_device_bf16,
                      run_gpu, to_device)
 
 pytestmark = pytest.mark.gpu
@@ -60,7 +60,7 @@ def run_reuse(qd, kd, vd, mask, tile_q, tile_k=TILE_K):
                            tile_k=tile_k, stats_out=stats, mask_out=mask_out, lse_out=lse,
                            mask_in=mask_in)
     torch.cuda.synchronize()
-    return GpuRun(from_device_bf16(o), mask_out.cpu().numpy().reshape(B, H, n_qu, n_kt),
+    return DeviceRun(from_device_bf16(o), mask_out.cpu().numpy().reshape(B, H, n_qu, n_kt),
                   lse.cpu().numpy().reshape(B, H, N), stats.cpu().numpy().reshape(B, H, 4))
 
 

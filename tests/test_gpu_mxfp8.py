@@ -25,7 +25,7 @@ from oracle import bf16_to_f64
 from oracle.mxfp8 import dequantize_mxfp8, key_mean, quantize_mxfp8, smooth_keys
 from synth import bf16_bits, make_random_qkv
 
-from _parity import (GpuRun, RULE_NAMES, assert_parity, compare, expected_stats_from_mask,
+from _parity import (DeviceRun, RULE_NAMES, assert_parity, compare, expected_stats_from_mask,
                      from_device_bf16, sample_tiles, to_device)
 
 pytestmark = pytest.mark.gpu
@@ -140,7 +140,7 @@ def run_gpu_q8(qc, qs, kc, ks, vd, rule, param, scale=SCALE, tile_q=128, key_ord
                               tile_q=tile_q, stats_out=stats, mask_out=mask, lse_out=lse,
                               key_order=key_order)
     torch.cuda.synchronize()
-    return GpuRun(from_device_bf16(o), mask.cpu().numpy().reshape(B, H, n_qt, n_kt),
+    return DeviceRun(from_device_bf16(o), mask.cpu().numpy().reshape(B, H, n_qt, n_kt),
                   lse.cpu().numpy().reshape(B, H, N), stats.cpu().numpy().reshape(B, H, 4))
 
 

@@ -20,7 +20,7 @@ import oracle
 from oracle.reorder import block_order, gather_rows, scatter_rows
 from synth import make_random_qkv, make_video_qkv
 
-from _parity import (GpuRun, RULE_NAMES, TILE_K, TILE_Q, assert_parity, compare,
+from _parity import (DeviceRun, RULE_NAMES, TILE_K, TILE_Q, assert_parity, compare,
                      expected_stats_from_mask, from_device_bf16, run_gpu, to_device)
 
 pytestmark = pytest.mark.gpu
@@ -137,7 +137,7 @@ def run_reordered(qd, kd, vd, rule, param, q_perm, kv_perm):
                                   dev_index(kv_perm), o, scale=SCALE, stats_out=stats,
                                   mask_out=mask, lse_out=lse)
     torch.cuda.synchronize()
-    return GpuRun(from_device_bf16(o), mask.cpu().numpy().reshape(B, H, n_qt, n_kt),
+    return DeviceRun(from_device_bf16(o), mask.cpu().numpy().reshape(B, H, n_qt, n_kt),
                   lse.cpu().numpy().reshape(B, H, N), stats.cpu().numpy().reshape(B, H, 4))
 
 
@@ -161,7 +161,7 @@ def test_reordered_attention_matches_oracle(grid, qb, kb, a, rule, param):
     g = run_reordered(to_device(q), to_device(k), to_device(v), rule, param, qp, kp)
     # the same problem in the reordered frame, on the oracle side
     qr, kr, vr = gather_rows(q, qp), gather_rows(k, kp), gather_rows(v, kp)
-    g_frame = GpuRun(gather_rows(g.o, qp), g.mask, gather_rows(g.lse[..., None], qp)[..., 0],
+    g_frame = DeviceRun(gather_rows(g.o, qp), g.mask, gather_rows(g.lse[..., None], qp)[..., 0],
                      g.stats)
     rep = compare(qr, kr, vr, g_frame, rule, param, SCALE)
     print(f"[case] {rep}", flush=True)
