@@ -107,25 +107,31 @@ __global__ __launch_bounds__(kThreads) void quantize_mxfp8_kernel(
   scales[blk] = (uint8_t)scode;
 }
 
-// Mean over the N keys of every head, one workgroup per head.  Thread t sums 16-byte
-// chunk t % (d / 8) of rows t / (d / 8), t / (d / 8) + P, ... (P = kMeanThreads / (d / 8)
-// rows in flight per step, eight steps unrolled), then the P partial sums of every column
-// are added in row order from LDS: a fixed order, so repeated calls agree bit for bit.
-constexpr int kMeanThreads = 1024;
+// Mean over the N keys of every head.  Workgroup (g, h) takes column group g of head h:
+// kMeanCols columns (64 bytes of every row; all of a row when d is smaller).  Thread t
+// sums 16-byte chunk t % C of rows t / C, t / C + P, ... (C chunks per group, P =
+// kMeanThreads / C rows in flight per step, eight steps unrolled); then the P partial sums
+// of every column are added in row order from LDS.  The order is fixed, so repeated
+// calls agree bit for bit.
+constexpr int kMeanThreads = 256;
+constexpr int kMeanCols = 32;
 
 __global__ __launch_bounds__(kMeanThreads) void key_mean_kernel(const u32x4* __restrict__ k,
                                                                 float* __restrict__ mean,
                                                                 int N, int d) {
   __shared__ float part[kMeanThreads * 8];
+  const int cols = d < kMeanCols ? d : kMeanCols;
+  const int cpg = cols >> 3;                 // 16-byte chunks per group and row
   const int cpr = d >> 3;                    // chunks per row
-  const int par = kMeanThreads / cpr;        // rows per step
+  const int par = kMeanThreads / cpg;        // rows per step
   const int t = threadIdx.x;
-  const int c = t % cpr;
-  const u32x4* base = k + (size_t)blockIdx.x * (size_t)N * cpr + c;
+  const int c = t % cpg;
+  const int head = blockIdx.y;
+  const u32x4* base = k + (size_t)head * (size_t)N * cpr + (size_t)blockIdx.x * cpg + c;
   float acc[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc[i] = 0.f;
-  int r = t / cpr;
+  int r = t / cpg;
   for (; r + 7 * par < N; r += 8 * par) {
     u32x4 x[8];
 #pragma unroll
@@ -150,11 +156,11 @@ __global__ __launch_bounds__(kMeanThreads) void key_mean_kernel(const u32x4* __r
   for (int i = 0; i < 8; ++i) part[t * 8 + i] = acc[i];
   __syncthreads();
   const float inv_n = 1.0f / (float)N;
-  for (int e = t; e < d; e += kMeanThreads) {
+  for (int e = t; e < cols; e += kMeanThreads) {
     const int ch = e >> 3, i = e & 7;
     float sum = 0.f;
-    for (int rl = 0; rl < par; ++rl) sum += part[(rl * cpr + ch) * 8 + i];
-    mean[(size_t)blockIdx.x * d + e] = sum * inv_n;
+    for (int rl = 0; rl < par; ++rl) sum += part[(rl * cpg + ch) * 8 + i];
+    mean[(size_t)head * d + (size_t)blockIdx.x * cols + e] = sum * inv_n;
   }
 }
 
@@ -179,8 +185,9 @@ hipError_t launch_quantize_mxfp8(const void* src, void* codes, void* scales,
 
 hipError_t launch_key_mean(const void* k, float* mean, int bh, int N, int d,
                            hipStream_t stream) {
-  hipLaunchKernelGGL(key_mean_kernel, dim3((unsigned)bh), dim3(kMeanThreads), 0, stream,
-                     static_cast<const u32x4*>(k), mean, N, d);
+  const int groups = d < kMeanCols ? 1 : d / kMeanCols;
+  hipLaunchKernelGGL(key_mean_kernel, dim3((unsigned)groups, (unsigned)bh), dim3(kMeanThreads),
+                     0, stream, static_cast<const u32x4*>(k), mean, N, d);
   return hipGetLastError();
 }
 
