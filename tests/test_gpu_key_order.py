@@ -162,3 +162,4 @@ def test_wan720p_sampled_diagonal():
         print(rep, f"full-run sparsity={float(g.mask.mean()):.4f}", flush=True)
         check(rep)
         assert (g.stats == expected_stats_from_mask(g.mask, w.N)).all()
+

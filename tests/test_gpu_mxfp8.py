@@ -339,3 +339,37 @@ def test_q8_attention_smoothed_keys(peaked_q8, rule, param):
         ref = bf16_to_f64(from_device_bf16(dsa.dense_attn_fwd(to_device(q), to_device(k), vd)))
         err = lambda x: np.linalg.norm(bf16_to_f64(x.o) - ref) / np.linalg.norm(ref)
         assert err(g) < 0.8 * err(plain), (err(g), err(plain))
+
+
+@pytest.mark.slow
+def test_q8_wan720p_sampled():
+    """The 720p layer with MX-FP8 Q and K quantised on the GPU (bit-exact with the oracle's
+    quantiser, as the tests above show): sampled query tiles of three heads against the
+    oracle on the dequantised values."""
+    import torch
+    import paper_2606_16317_amd as dsa
+    from synth import WORKLOADS, workload_inputs
+
+    from _parity import sample_tiles
+
+    w = WORKLOADS["wan720p"]
+    announce(f"generate {w.describe()}")
+    q, k, v, _ = workload_inputs("wan720p")
+    qd, kd, vd = to_device(q), to_device(k), to_device(v)
+    qc, qs = dsa.dsattn_quantize_mxfp8(qd)
+    kc, ks = dsa.dsattn_quantize_mxfp8(kd)
+    del qd, kd
+    heads = [(0, 1), (0, 20), (0, 33)]
+    tiles = sample_tiles(w.B, w.H, w.N, per_head=3, heads=heads, seed=6)
+    qf = np.zeros(q.shape, np.float64)
+    kf = np.zeros(k.shape, np.float64)
+    for (b, h) in heads:                       # dequantise the sampled heads only
+        qf[b, h] = dequantize_mxfp8(qc[b, h].cpu().numpy(), qs[b, h].cpu().numpy())
+        kf[b, h] = dequantize_mxfp8(kc[b, h].cpu().numpy(), ks[b, h].cpu().numpy())
+    for rule, param in [("dynsparse_lambda", -6.0), ("dynsparse_recall", 0.95)]:
+        announce(f"q8 wan720p rule={rule} param={param} tiles={len(tiles)}")
+        g = run_gpu_q8(qc, qs, kc, ks, vd, rule, param)
+        rep = compare(qf, kf, v, g, rule, param, SCALE, tiles=tiles)
+        print(rep, f"full-run tile sparsity={float(g.mask.mean()):.4f}", flush=True)
+        assert_parity(rep)
+        assert (g.stats == expected_stats_from_mask(g.mask, w.N)).all()
