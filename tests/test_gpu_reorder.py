@@ -200,3 +200,30 @@ def test_reordering_raises_sparsity_on_video_inputs():
     print(f"[case] sparsity row-major {plain.mask.mean():.3f} reordered {r.mask.mean():.3f}",
           flush=True)
     assert r.mask.mean() > plain.mask.mean()
+
+
+@pytest.mark.slow
+def test_reordered_wan720p_sampled():
+    """The 720p layer regrouped into (2, 8, 8) query and (1, 8, 8) key/value blocks, in
+    the launch shape the reorder sweep times: sampled query tiles of three heads against
+    the oracle in the reordered frame."""
+    from synth import WORKLOADS, workload_inputs
+
+    from _parity import sample_tiles
+
+    w = WORKLOADS["wan720p"]
+    announce(f"generate {w.describe()}")
+    q, k, v, _ = workload_inputs("wan720p")
+    qp, kp = block_order(w.grid, (2, 8, 8)), block_order(w.grid, (1, 8, 8))
+    dev = (to_device(q), to_device(k), to_device(v))
+    qr, kr, vr = gather_rows(q, qp), gather_rows(k, kp), gather_rows(v, kp)
+    tiles = sample_tiles(w.B, w.H, w.N, per_head=3, heads=[(0, 2), (0, 21), (0, 39)], seed=7)
+    for rule, param in [("dynsparse_lambda", -8.0), ("dynsparse_recall", 0.95)]:
+        announce(f"reordered wan720p rule={rule} param={param} tiles={len(tiles)}")
+        g = run_reordered(*dev, rule, param, qp, kp)
+        g_frame = DeviceRun(gather_rows(g.o, qp), g.mask,
+                            gather_rows(g.lse[..., None], qp)[..., 0], g.stats)
+        rep = compare(qr, kr, vr, g_frame, rule, param, SCALE, tiles=tiles)
+        print(rep, f"full-run tile sparsity={float(g.mask.mean()):.4f}", flush=True)
+        assert_parity(rep)
+        assert np.array_equal(g.stats, expected_stats_from_mask(g.mask, w.N))
