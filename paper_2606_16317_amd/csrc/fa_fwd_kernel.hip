@@ -363,6 +363,7 @@ struct RowState {
   float m_ref;   // reference max (log2 units) of P = exp2(S*c - m_ref)
   float m_true;  // running max of the kept tiles (BLASST metric)
   float l_half;  // this lane's share of the kept row sum, relative to m_ref
+  float lse;     // MX-FP8 64-key steps: m_ref + log2(row sum) after the last kept tile
 };
 
 // Lazy rescale at the start of a kept tile with row max m_hat (log2 units).
@@ -518,6 +519,16 @@ __device__ __forceinline__ bool row_keeps(const RowState& rs, float m_hat, float
   }
 }
 
+// The same against the LSE cached in rs.lse.  The LSE changes only when a tile is kept,
+// so a run of skipped tiles reuses it instead of recomputing it before every vote.
+template <int RULE>
+__device__ __forceinline__ bool row_keeps_cached(const RowState& rs, float m_hat, float thr) {
+  if constexpr (RULE == kRuleDynSparse)
+    return !(m_hat - rs.lse < thr);
+  else
+    return !(m_hat - rs.m_true < thr);
+}
+
 // Per-thread constants of the key-tile loop.
 struct LoopCtx {
   __amdgpu_buffer_rsrc_t krs;   // K / V of this head as buffer resources
@@ -663,6 +674,10 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
     else
       kept_tile(rs, o, s_cur, mhat, cx.c, s_next, sm.k[nb], sm.v[j & 1], qf, cx.r, cx.g,
                 cx.lane);
+    // The MX-FP8 path caches the LSE for its votes (its kept tiles are shorter, and taking
+    // the log out of the vote chain pays there); the bf16 path keeps it in the chain.
+    if constexpr (Q8 && RULE == kRuleDynSparse)
+      rs.lse = rs.m_ref + log2_fast(half_sum(rs.l_half));
   } else {
     sk.tiles += 1;
     sk.elems += (uint64_t)cx.rows_valid * (uint64_t)min(kTK, cx.N - tj * kTK);
@@ -680,7 +695,8 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
     if (cx.ragged && tn == cx.n_kt - 1) mask_tail(s_next, tn * kTK, cx.N, cx.g);
     mhat_next = row_max(s_next) * cx.c;
     if constexpr (RULE != kRuleDense) {
-      wave_keeps = __ballot(cx.valid & row_keeps<RULE>(rs, mhat_next, cx.thr)) != 0;
+      wave_keeps = __ballot(cx.valid & (Q8 ? row_keeps_cached<RULE>(rs, mhat_next, cx.thr)
+                                              : row_keeps<RULE>(rs, mhat_next, cx.thr))) != 0;
       const uint32_t mark = wave_keeps ? 0u : 1u;
       if (mark != ((marks >> nb) & 1u)) {
         if (cx.lane == 0) sm.vote[nb][cx.w] = (uint8_t)mark;
@@ -1211,7 +1227,7 @@ fa_fwd_kernel(FwdParams p) {
   f32x16 o[4];
 #pragma unroll
   for (int db = 0; db < 4; ++db) o[db] = f32x16{};
-  RowState rs{-__builtin_inff(), -__builtin_inff(), 0.f};
+  RowState rs{-__builtin_inff(), -__builtin_inff(), 0.f, -__builtin_inff()};
 
   load_k_tile<Q8>(sm, 1, cx, (PAIR ? pair_tile<ORDER>(1, cx) : key_tile_or_past<ORDER>(1, cx)) * kTK);
   if (cx.lane == 0) {                        // vote bytes start at 0 (not skipping)
@@ -1451,7 +1467,7 @@ fa_fwd_mask_kernel(FwdParams p) {
   f32x16 o[4];
 #pragma unroll
   for (int db = 0; db < 4; ++db) o[db] = f32x16{};
-  RowState rs{-__builtin_inff(), -__builtin_inff(), 0.f};
+  RowState rs{-__builtin_inff(), -__builtin_inff(), 0.f, -__builtin_inff()};
 
   if (n_keep > 0) {
     const int t0 = list_tile(sm, 0);
