@@ -391,6 +391,17 @@ __device__ __forceinline__ void softmax_elem(const f32x16 (&st)[2], int e, float
   pf[2 * b + (v >> 3)][v & 7] = (__bf16)x;
 }
 
+// Softmax numerator of element e without the row sum: the value is kept in xs[e] and
+// added up after the P V MFMAs are issued, in element order.
+__device__ __forceinline__ void softmax_elem_keep(const f32x16 (&st)[2], int e, float c,
+                                                  float neg_m, float (&xs)[32],
+                                                  bf16x8 (&pf)[4]) {
+  const int b = e >> 4, v = e & 15;
+  const float x = exp2_fast(fmaf(st[b][v], c, neg_m));
+  xs[e] = x;
+  pf[2 * b + (v >> 3)][v & 7] = (__bf16)x;
+}
+
 // Kept tile j: softmax of S_j interleaved with the 16 MFMAs of S_{j+1} = K_{j+1} Q^T,
 // then O += P V_j.  MFMA operands are read from LDS two MFMAs ahead.
 __device__ __forceinline__ void kept_tile(RowState& rs, f32x16 (&o)[4], const f32x16 (&s_cur)[2],
@@ -403,7 +414,7 @@ __device__ __forceinline__ void kept_tile(RowState& rs, f32x16 (&o)[4], const f3
   // sum stay as they are.
   if (contribute) rescale_if_needed(rs, o, m_hat);
   const float neg_m = contribute ? -rs.m_ref : -__builtin_inff();
-  float psum = 0.f;
+  float xs[32];
   bf16x8 pf[4];
   bf16x8 ka[3], va[3];
   ka[0] = k_operand(kt, 0, r, g);
@@ -419,11 +430,10 @@ __device__ __forceinline__ void kept_tile(RowState& rs, f32x16 (&o)[4], const f3
     f32x16& acc = s_next[i & 1];
     acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[i % 3], qf[i >> 1],
                                                   i < 2 ? f32x16{} : acc, 0, 0, 0);
-    softmax_elem(s_cur, 2 * i, c, neg_m, psum, pf);
-    softmax_elem(s_cur, 2 * i + 1, c, neg_m, psum, pf);
+    softmax_elem_keep(s_cur, 2 * i, c, neg_m, xs, pf);
+    softmax_elem_keep(s_cur, 2 * i + 1, c, neg_m, xs, pf);
     sched_fence();
   }
-  rs.l_half += psum;
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     if (i + 2 < 16) va[(i + 2) % 3] = v_operand(vt, i + 2, lane);
@@ -431,6 +441,12 @@ __device__ __forceinline__ void kept_tile(RowState& rs, f32x16 (&o)[4], const f3
     sched_fence();
   }
   __builtin_amdgcn_s_setprio(0);
+  // The row sum goes after the P V MFMAs, where the VALU is otherwise idle, rather than
+  // into the softmax phase, which is VALU-bound.
+  float psum = 0.f;
+#pragma unroll
+  for (int e = 0; e < 32; ++e) psum += xs[e];
+  rs.l_half += psum;
 }
 
 // Kept tile j on the MX-FP8 path: as kept_tile, with S_{j+1} from four scaled fp8 MFMAs
