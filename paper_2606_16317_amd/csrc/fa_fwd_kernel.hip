@@ -459,7 +459,7 @@ __device__ __forceinline__ void kept_tile_q8(RowState& rs, f32x16 (&o)[4],
                                              const QFrag8& qf, int r, int g, int lane) {
   rescale_if_needed(rs, o, m_hat);
   const float neg_m = -rs.m_ref;
-  float psum = 0.f;
+  float xs[32];
   bf16x8 pf[4];
   bf16x8 va[3];
   KFrag8 kf;
@@ -471,10 +471,9 @@ __device__ __forceinline__ void kept_tile_q8(RowState& rs, f32x16 (&o)[4],
     qk_q8_step(i, s_next, kf, kt, qf, r, g);
     if (i >= 2) va[i - 2] = v_operand(vt, i - 2, lane);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) softmax_elem(s_cur, 8 * i + e, c, neg_m, psum, pf);
+    for (int e = 0; e < 8; ++e) softmax_elem_keep(s_cur, 8 * i + e, c, neg_m, xs, pf);
     sched_fence();
   }
-  rs.l_half += psum;
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     if (i + 2 < 16) va[(i + 2) % 3] = v_operand(vt, i + 2, lane);
@@ -482,6 +481,10 @@ __device__ __forceinline__ void kept_tile_q8(RowState& rs, f32x16 (&o)[4],
     sched_fence();
   }
   __builtin_amdgcn_s_setprio(0);
+  float psum = 0.f;                          // after the P V MFMAs, as in kept_tile
+#pragma unroll
+  for (int e = 0; e < 32; ++e) psum += xs[e];
+  rs.l_half += psum;
 }
 
 // Skipped tile j: only S_{j+1} = K_{j+1} Q^T.
