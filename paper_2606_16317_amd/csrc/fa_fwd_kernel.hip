@@ -430,14 +430,21 @@ __device__ __forceinline__ void kept_tile(RowState& rs, f32x16 (&o)[4], const f3
     f32x16& acc = s_next[i & 1];
     acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[i % 3], qf[i >> 1],
                                                   i < 2 ? f32x16{} : acc, 0, 0, 0);
-    softmax_elem_keep(s_cur, 2 * i, c, neg_m, xs, pf);
-    softmax_elem_keep(s_cur, 2 * i + 1, c, neg_m, xs, pf);
+    // elements 0-23 here: two under each of the first eight MFMAs, one under the rest
+    if (i < 8) {
+      softmax_elem_keep(s_cur, 2 * i, c, neg_m, xs, pf);
+      softmax_elem_keep(s_cur, 2 * i + 1, c, neg_m, xs, pf);
+    } else {
+      softmax_elem_keep(s_cur, 16 + (i - 8), c, neg_m, xs, pf);
+    }
     sched_fence();
   }
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     if (i + 2 < 16) va[(i + 2) % 3] = v_operand(vt, i + 2, lane);
     o[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i % 3], pf[i >> 2], o[i & 3], 0, 0, 0);
+    // elements 24-31 (P block 3, first read by MFMA 12) under the first eight
+    if (i < 8) softmax_elem_keep(s_cur, 24 + i, c, neg_m, xs, pf);
     sched_fence();
   }
   __builtin_amdgcn_s_setprio(0);
