@@ -478,13 +478,14 @@ __device__ __forceinline__ void kept_tile_q8(RowState& rs, f32x16 (&o)[4],
     qk_q8_step(i, s_next, kf, kt, qf, r, g);
     if (i >= 2) va[i - 2] = v_operand(vt, i - 2, lane);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) softmax_elem_keep(s_cur, 8 * i + e, c, neg_m, xs, pf);
+    for (int e = 0; e < 6; ++e) softmax_elem_keep(s_cur, 6 * i + e, c, neg_m, xs, pf);
     sched_fence();
   }
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     if (i + 2 < 16) va[(i + 2) % 3] = v_operand(vt, i + 2, lane);
     o[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i % 3], pf[i >> 2], o[i & 3], 0, 0, 0);
+    if (i < 8) softmax_elem_keep(s_cur, 24 + i, c, neg_m, xs, pf);   // P block 3, as in kept_tile
     sched_fence();
   }
   __builtin_amdgcn_s_setprio(0);
