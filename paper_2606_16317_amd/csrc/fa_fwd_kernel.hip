@@ -24,15 +24,18 @@
 // which is what one ds_read_b64_tr_b16 delivers from a row-major V tile.
 //
 // Pipeline (one barrier per key tile): S_{j+1} is computed during iteration j, so the
-// decision for tile j+1 is voted before the barrier that closes iteration j and read
-// right after it (the read's latency overlaps the issue of the next K-tile DMA).  K is
+// decision for tile j+1 is voted before the barrier that closes iteration j.  A wave
+// writes its vote byte only when its vote changes, and only waves that vote skip read
+// the others' after the barrier (the read's latency overlaps the issue of the next K-tile
+// DMA), so with nothing skipped the votes touch no LDS.  K is
 // prefetched two tiles ahead and V one tile ahead, straight from global memory into LDS
 // (buffer loads with the LDS bit; rows past the sequence end come back as zeros from the
 // buffer range check); V is fetched only for tiles that follow a kept tile or are
 // themselves kept, so runs of skipped tiles stream K alone.  Inside an iteration the
-// instruction order is fixed by scheduling fences: each of the 16 S_{j+1} MFMAs carries
-// two elements of the tile-j softmax, and MFMA operands are read from LDS two MFMAs
-// ahead.
+// instruction order is fixed by scheduling fences: the 16 S_{j+1} MFMAs carry 24 elements
+// of the tile-j softmax and the first eight P V MFMAs the other 8 (the ones the last four
+// P V MFMAs read); the row sum is added after the P V MFMAs, where the VALU is otherwise
+// idle; MFMA operands are read from LDS two MFMAs ahead.
 //
 // Variants, all compile-time parameters of fa_fwd_kernel:
 //   * UNIT: the query rows that share a decision, the workgroup's 128 or each wave's 32;
@@ -79,7 +82,7 @@ constexpr float kRescaleSlack = 8.0f;        // log2 units
 struct Smem {
   alignas(16) uint16_t k[2][kTileElems];     // bf16 K tiles, or MX-FP8 K tiles (first half)
   alignas(16) uint16_t v[2][kTileElems];
-  alignas(4) uint8_t vote[2][kWaves];        // one byte per wave, read back as one dword
+  alignas(4) uint8_t vote[2][kWaves];        // per wave: 1 while its last vote here was skip
   alignas(16) uint8_t ks[2][kTK * 4];        // MX-FP8 K: E8M0 exponents, 4 blocks per key
   alignas(4) uint8_t vote_h1[2][kWaves];     // B_c = 32: second-half votes
   alignas(4) uint8_t vote_mid[kWaves];       // B_c = 32: second-half votes taken mid-step
