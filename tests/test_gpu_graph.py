@@ -118,3 +118,88 @@ def test_quantise_and_q8_attention_replays_match_eager():
         torch.cuda.synchronize()
         for a, b in zip(got, (o, st, mk, ls)):
             assert torch.equal(a, b), rep
+
+
+def test_diagonal_rule_then_mask_reuse_replays_match_eager():
+    """One graph holding a DynSparse call in diagonal-first order that writes its mask and
+    a mask-reuse call that consumes it: every replay (new inputs each time) equals the
+    same two calls run eagerly."""
+    import torch
+    import paper_2606_16317_amd as dsa
+
+    announce("graph: diagonal-order rule call, then mask reuse")
+    B, H, N = 1, 3, 1000
+    inputs = [make_video_qkv(B, H, (2, 10, 50), 5.0, 5.0, True, s)[:3] for s in (4, 5, 6)]
+    qd, kd, vd = (to_device(x) for x in inputs[0])
+
+    def bufs():
+        return (buffers(B, H, N), buffers(B, H, N))
+
+    def pipeline(q, k, v, first, second):
+        o1, st1, mk1, ls1 = first
+        o2, st2, mk2, ls2 = second
+        dsa.dsattn_attn_fwd_ex(dsa.RULE_DYNSPARSE_LAMBDA, -6.0, q, k, v, o1, scale=SCALE,
+                               stats_out=st1, mask_out=mk1, lse_out=ls1,
+                               key_order=dsa.ORDER_DIAGONAL)
+        dsa.dsattn_attn_fwd_ex(dsa.RULE_MASK, 0.0, q, k, v, o2, scale=SCALE, stats_out=st2,
+                               mask_out=mk2, lse_out=ls2, mask_in=mk1)
+
+    first, second = bufs()
+    pipeline(qd, kd, vd, first, second)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        pipeline(qd, kd, vd, first, second)
+    for rep in range(4):
+        q, k, v = inputs[rep % 3]
+        qd.copy_(to_device(q)); kd.copy_(to_device(k)); vd.copy_(to_device(v))
+        for t in first + second:
+            t.zero_()
+        g.replay()
+        ref_first, ref_second = bufs()
+        pipeline(to_device(q), to_device(k), to_device(v), ref_first, ref_second)
+        torch.cuda.synchronize()
+        for got, want in zip(first + second, ref_first + ref_second):
+            assert torch.equal(got, want), rep
+        assert float(first[2].float().mean()) > 0.05           # the first call skipped
+
+
+def test_reordered_attention_replays_match_eager():
+    """The reordered entry point (row gathers, the rule, the output scatter) captured with
+    a caller-provided workspace: replays equal eager calls."""
+    import torch
+    import paper_2606_16317_amd as dsa
+
+    announce("graph: reordered attention")
+    B, H, N, grid = 1, 2, 1000, (2, 10, 50)
+    inputs = [make_video_qkv(B, H, grid, 5.0, 5.0, True, s)[:3] for s in (7, 8, 9)]
+    qd, kd, vd = (to_device(x) for x in inputs[0])
+    qi = torch.from_numpy(dsa.dsattn_block_order(grid, (2, 8, 8))).cuda()
+    ki = torch.from_numpy(dsa.dsattn_block_order(grid, (1, 8, 8))).cuda()
+    ws = torch.empty(dsa.dsattn_reordered_workspace_bytes(B, H, N, 128, True),
+                     dtype=torch.uint8, device="cuda")
+    ws_ref = torch.empty_like(ws)
+
+    def call(q, k, v, out, work):
+        o, st, mk, ls = out
+        dsa.dsattn_attn_fwd_reordered(dsa.RULE_DYNSPARSE_LAMBDA, -6.0, q, k, v, qi, ki, o,
+                                      scale=SCALE, stats_out=st, mask_out=mk, lse_out=ls,
+                                      workspace=work)
+
+    out = buffers(B, H, N)
+    call(qd, kd, vd, out, ws)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        call(qd, kd, vd, out, ws)
+    for rep in range(4):
+        q, k, v = inputs[rep % 3]
+        qd.copy_(to_device(q)); kd.copy_(to_device(k)); vd.copy_(to_device(v))
+        for t in out:
+            t.zero_()
+        g.replay()
+        ref = buffers(B, H, N)
+        call(to_device(q), to_device(k), to_device(v), ref, ws_ref)
+        torch.cuda.synchronize()
+        for got, want in zip(out, ref):
+            assert torch.equal(got, want), rep
