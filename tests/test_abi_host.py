@@ -368,3 +368,36 @@ def test_key_tile_restrictions():
     a.qk_format, a.key_order = 0, pkg.ORDER_DIAGONAL
     assert L.dsattn_attn_fwd_ex(ctypes.byref(a)) == -2
     assert "ascending" in pkg.last_error()
+
+
+def test_last_error_is_per_thread():
+    """dsattn_last_error belongs to the calling thread: threads that fail with different
+    arguments each read their own message, and a thread whose call succeeds reads ""."""
+    import threading
+
+    pkg = _lib()
+    L = pkg.lib()
+    results = {}
+    barrier = threading.Barrier(3)
+
+    def worker(name, call):
+        barrier.wait()
+        out = []
+        for _ in range(200):
+            rc = call()
+            out.append((rc, pkg.last_error()))
+        results[name] = out
+
+    calls = {
+        "recall": lambda: _fwd("dynsparse_attn_fwd", 1.5)[0],            # bad recall
+        "head": lambda: L.dsattn_key_mean(None, None, 1, 4, 12, None),  # bad d
+        "ok": lambda: L.dsattn_key_mean(None, None, 0, 4, 128, None),   # empty: success
+    }
+    threads = [threading.Thread(target=worker, args=(n, c)) for n, c in calls.items()]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert all(rc == -1 and "recall" in msg for rc, msg in results["recall"])
+    assert all(rc == -1 and "power of two" in msg for rc, msg in results["head"])
+    assert all(rc == 0 and msg == "" for rc, msg in results["ok"])

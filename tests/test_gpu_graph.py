@@ -203,3 +203,41 @@ def test_reordered_attention_replays_match_eager():
         torch.cuda.synchronize()
         for got, want in zip(out, ref):
             assert torch.equal(got, want), rep
+
+
+def test_calls_on_two_streams_match_serial_calls():
+    """Two different problems enqueued on two streams at once (default priority) give the
+    same bits as the same calls run one after the other: the library keeps no state
+    between calls besides the caller's buffers."""
+    import torch
+    import paper_2606_16317_amd as dsa
+
+    announce("two streams")
+    B, H, N = 1, 3, 1000
+    a = [to_device(x) for x in make_video_qkv(B, H, (2, 10, 50), 5.0, 5.0, True, 11)[:3]]
+    b = [to_device(x) for x in make_video_qkv(B, H, (2, 10, 50), 3.0, 3.0, True, 12)[:3]]
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    out_a, out_b = buffers(B, H, N), buffers(B, H, N, tile_q=32)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        with torch.cuda.stream(s1):
+            o, st, mk, ls = out_a
+            dsa.dsattn_attn_fwd_ex(dsa.RULE_DYNSPARSE_LAMBDA, -6.0, *a, o, scale=SCALE,
+                                   stats_out=st, mask_out=mk, lse_out=ls,
+                                   stream=s1)
+        with torch.cuda.stream(s2):
+            o, st, mk, ls = out_b
+            dsa.dsattn_attn_fwd_ex(dsa.RULE_BLASST, 1e-2, *b, o, scale=SCALE, tile_q=32,
+                                   stats_out=st, mask_out=mk, lse_out=ls,
+                                   stream=s2)
+    torch.cuda.synchronize()
+    ref_a, ref_b = buffers(B, H, N), buffers(B, H, N, tile_q=32)
+    o, st, mk, ls = ref_a
+    dsa.dsattn_attn_fwd_ex(dsa.RULE_DYNSPARSE_LAMBDA, -6.0, *a, o, scale=SCALE, stats_out=st,
+                           mask_out=mk, lse_out=ls)
+    o, st, mk, ls = ref_b
+    dsa.dsattn_attn_fwd_ex(dsa.RULE_BLASST, 1e-2, *b, o, scale=SCALE, tile_q=32, stats_out=st,
+                           mask_out=mk, lse_out=ls)
+    torch.cuda.synchronize()
+    for got, want in zip(out_a + out_b, ref_a + ref_b):
+        assert torch.equal(got, want)
