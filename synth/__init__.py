@@ -14,6 +14,7 @@ from .video_qkv import (
     make_video_qkv,
     workload_inputs,
 )
+from .margin_band import margin_band_inputs
 from .vote_patterns import expected_skip, vote_pattern_inputs
 
 __all__ = [
@@ -25,5 +26,6 @@ __all__ = [
     "make_video_qkv",
     "workload_inputs",
     "vote_pattern_inputs",
+    "margin_band_inputs",
     "expected_skip",
 ]

@@ -98,6 +98,7 @@ class Report:
     rel_l2_vs_dense: float
     sparsity: float
     lse_max_err: float
+    near: int = 0          # pairs whose oracle margin lies within the tolerance band
 
 
 def compare(q, k, v, g: DeviceRun, rule: str, param: float, scale: float, tiles=None,
@@ -108,7 +109,7 @@ def compare(q, k, v, g: DeviceRun, rule: str, param: float, scale: float, tiles=
     name, thr = oracle_rule(rule, param, N)
     run = oracle.rule_attention(q, k, v, scale, name, thr, tile_q, tile_k, tiles=tiles,
                                 forced_mask=g.mask, key_order=key_order)
-    mism, worst = 0, 0.0
+    mism, worst, near = 0, 0.0, 0
     num = den = dnum = 0.0
     max_abs = lse_err = 0.0
     pairs = 0
@@ -116,6 +117,7 @@ def compare(q, k, v, g: DeviceRun, rule: str, param: float, scale: float, tiles=
         own = res.margin < 0
         bad = own != res.skip
         mism += int(bad.sum())
+        near += int((np.abs(res.margin) < MARGIN_TOL).sum())
         if bad.any():
             worst = max(worst, float(np.abs(res.margin[bad]).max()))
         pairs += res.skip.size
@@ -129,7 +131,7 @@ def compare(q, k, v, g: DeviceRun, rule: str, param: float, scale: float, tiles=
     dden = sum(float((r.o_dense ** 2).sum()) for r in run.results)
     return Report(len(run.tiles), pairs, mism, worst, max_abs, math.sqrt(num / den),
                   math.sqrt(dnum / dden), float(np.mean([r.skip.mean() for r in run.results])),
-                  lse_err)
+                  lse_err, near)
 
 
 def assert_parity(rep: Report):

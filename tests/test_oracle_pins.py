@@ -166,6 +166,98 @@ def test_brute_force_actually_skips():
 
 
 # ---------------------------------------------------------------------------------------
+# P2b: exact ties.  Section 3.1 skips a tile only when its metric is strictly below the
+# threshold, so t == threshold keeps it.  Every case below is built from values that are
+# exact in binary floating point (logits 0, -0.5, -0.75; a single zero logit has LSE 0;
+# the running max of zero logits is 0), so the tie is exact and a "<=" comparison would
+# give a different answer in each one.
+
+def _next_up(x):
+    return float(np.nextafter(x, math.inf))
+
+
+def _next_down(x):
+    return float(np.nextafter(x, -math.inf))
+
+
+def test_tie_keeps_tile_dynsparse_single_keys():
+    """Single-key tiles, two rows.  After tile 0 (logit 0) the LSE of both rows is 0, so
+    tile 1 has t = (-0.5, -0.75) and the unit's metric is max_r t = -0.5."""
+    s = np.array([[0.0, -0.5], [0.0, -0.75]])
+    v = np.array([[1.0, 0.0], [0.0, 1.0]])
+    at = filter_q_tile(s, v, "dynsparse", -0.5, 1)
+    assert list(at.skip) == [False, False]           # t == lambda: kept
+    assert at.margin[1] == 0.0
+    assert list(filter_q_tile(s, v, "dynsparse", _next_up(-0.5), 1).skip) == [False, True]
+    assert list(filter_q_tile(s, v, "dynsparse", _next_down(-0.5), 1).skip) == [False, False]
+    # the kept tile enters the LSE: row 0 keeps e^0 + e^-0.5 of its mass
+    np.testing.assert_allclose(at.lse_kept[0], math.log(1.0 + math.exp(-0.5)), rtol=1e-15)
+
+
+def test_tie_keeps_tile_blasst_single_keys():
+    """BLASST on the same logits: the running max after tile 0 is 0, so tile 1 has
+    t = (-0.5, -0.75); ln(tau) = -0.5 is a tie and keeps it."""
+    s = np.array([[0.0, -0.5], [0.0, -0.75]])
+    v = np.eye(2)
+    assert list(filter_q_tile(s, v, "blasst", -0.5, 1).skip) == [False, False]
+    assert list(filter_q_tile(s, v, "blasst", _next_up(-0.5), 1).skip) == [False, True]
+
+
+def test_tie_keeps_tile_uniform_dynsparse_full_pipeline():
+    """Q = 0 from bf16 inputs, single-key tiles, lambda = 0: tile 1 has t = 0 - ln(1) = 0,
+    a tie, and is kept; from tile 2 on t = -ln 2 < 0.  So exactly tiles 0 and 1 are kept
+    (a strict "<" is the only comparison that keeps two), the recall is 2/N and the output
+    is the mean of the first two value rows."""
+    n = 8
+    q = np.zeros((1, 1, n, 4), np.uint16)          # bf16 +0
+    k = bf16_bits(np.arange(n * 4, dtype=np.float32).reshape(1, 1, n, 4) / 7)
+    v = bf16_bits(np.random.default_rng(3).standard_normal((1, 1, n, 4)).astype(np.float32))
+    run = rule_attention(q, k, v, 1.0, "dynsparse", 0.0, n, 1)
+    res = run.results[0]
+    assert list(np.nonzero(~res.skip)[0]) == [0, 1]
+    assert res.margin[1] == 0.0
+    np.testing.assert_allclose(res.recall, 2.0 / n, rtol=1e-15)
+    vv = f64(v[0, 0])
+    np.testing.assert_allclose(res.o_sparse, np.tile((vv[0] + vv[1]) / 2, (n, 1)), rtol=1e-15)
+
+
+def test_tie_keeps_every_tile_blasst_tau_one_full_pipeline():
+    """Uniform logits under BLASST with tau = 1: every tile has t = 0 - 0 = ln(1), a tie,
+    so nothing is skipped and the output is dense attention (the mean of V)."""
+    n = 96
+    q = np.zeros((1, 1, n, 8), np.uint16)
+    k = bf16_bits(np.random.default_rng(4).standard_normal((1, 1, n, 8)).astype(np.float32))
+    v = bf16_bits(np.random.default_rng(5).standard_normal((1, 1, n, 8)).astype(np.float32))
+    run = rule_attention(q, k, v, 0.5, "blasst", log_threshold_blasst(1.0), 32, 16)
+    assert all(not r.skip.any() for r in run.results)
+    for r in run.results:
+        assert r.margin[0] == math.inf and (r.margin[1:] == 0.0).all()
+    mean = f64(v[0, 0]).mean(axis=0)
+    for r in run.results:
+        np.testing.assert_allclose(r.o_sparse, np.tile(mean, (r.o_sparse.shape[0], 1)),
+                                   rtol=1e-13, atol=1e-15)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_blasst_integer_logit_ties_match_brute_force(seed):
+    """Integer logits and integer thresholds: BLASST's metric m_hat - m is an integer, so
+    exact ties occur throughout; the streaming oracle equals the from-scratch brute force
+    (which keeps a tile unless t < threshold) and ties do occur."""
+    rng = np.random.default_rng(200 + seed)
+    s = rng.integers(-4, 1, size=(3, 24)).astype(np.float64)
+    v = rng.standard_normal((24, 3))
+    ties = 0
+    for thr in (-1.0, -2.0, -3.0):
+        for tk in (1, 2, 3):
+            res = filter_q_tile(s, v, "blasst", thr, tk)
+            skip, kept = brute_force_rule(s.tolist(), "blasst", thr, tk)
+            assert np.array_equal(res.skip, skip)
+            assert list(res.kept_cols) == kept
+            ties += int((res.margin == 0.0).sum())
+    assert ties > 0
+
+
+# ---------------------------------------------------------------------------------------
 # P3/P4: the recall theorem of Section 3.1
 
 def _concentrated_inputs(a, seed, grid=(2, 16, 32)):
