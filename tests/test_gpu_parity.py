@@ -209,49 +209,88 @@ def test_binding_rejects_host_and_wrong_dtype(gpu):
 
 # ---------------------------------------------------------------------------------------
 # full-size workloads, sampled Q tiles (the launch shapes the bench times)
+#
+# Per workload and rule: 6 query tiles of each of 3-4 sampled heads -- the first, the
+# last (ragged) and 4 drawn from the interior -- every key tile of each.  One workload's
+# inputs are held at a time.
 
-def _full(name, rules, per_head=2, n_heads=4, seed=0):
-    w = WORKLOADS[name]
-    announce(f"generate {w.describe()}")
-    q, k, v, meta = workload_inputs(name)
-    dev = upload(q, k, v)
+_HELD = {}
+
+
+def _workload(name):
+    if name not in _HELD:
+        _HELD.clear()
+        w = WORKLOADS[name]
+        announce(f"generate {w.describe()}")
+        q, k, v, meta = workload_inputs(name)
+        _HELD[name] = (w, (q, k, v), upload(q, k, v))
+    return _HELD[name]
+
+
+def _full(name, rule, param, n_heads=4, per_head=6, seed=0):
+    w, (q, k, v), dev = _workload(name)
     heads = [(b, h) for b in range(w.B) for h in range(w.H)]
     rng = np.random.default_rng(seed)
     pick = [heads[i] for i in sorted(rng.choice(len(heads), size=min(n_heads, len(heads)),
                                                 replace=False))]
     tiles = sample_tiles(w.B, w.H, w.N, per_head=per_head, heads=pick, seed=seed)
-    for rule, param in rules:
-        announce(f"{name} rule={rule} param={param} tiles={len(tiles)}")
-        g = run_gpu(*dev, rule, param, SCALE)
-        rep = compare(q, k, v, g, rule, param, SCALE, tiles=tiles)
-        full_sp = float(g.mask.mean())
-        print(rep, f"full-run tile sparsity={full_sp:.4f}", flush=True)
-        assert_parity(rep)
-        assert (g.stats == expected_stats_from_mask(g.mask, w.N)).all()
-    del dev
+    n_qt = -(-w.N // TILE_Q)
+    assert any(0 < qi < n_qt - 1 for (_, _, qi) in tiles)      # interior tiles sampled
+    announce(f"{name} rule={rule} param={param} tiles={len(tiles)}")
+    g = run_gpu(*dev, rule, param, SCALE)
+    rep = compare(q, k, v, g, rule, param, SCALE, tiles=tiles)
+    full_sp = float(g.mask.mean())
+    print(rep, f"mismatches={rep.mismatches} within_band={rep.near} "
+               f"full-run tile sparsity={full_sp:.4f}", flush=True)
+    assert_parity(rep)
+    assert (g.stats == expected_stats_from_mask(g.mask, w.N)).all()
+    return g, tiles
+
+
+def _has_mixed_runs(g, tiles):
+    """Some sampled tile keeps a key tile right after skipping one (the late-V path)."""
+    for (b, h, qi) in tiles:
+        m = g.mask[b, h, qi].astype(bool)
+        if (m[:-1] & ~m[1:]).any():
+            return True
+    return False
+
+
+FULL_CASES = [
+    ("wan480p", "dynsparse_recall", 0.95, 4, 1),
+    ("wan480p", "dynsparse_lambda", -8.0, 4, 1),
+    ("wan720p", "dynsparse_recall", 0.95, 4, 2),
+    ("wan720p", "dense", 0.0, 4, 2),
+    ("wan720p", "dynsparse_lambda", -8.0, 4, 2),
+    ("wan720p", "dynsparse_lambda", -6.0, 4, 2),
+    # the threshold sweep draw: every point of the sweep (recall targets, BLASST
+    # thresholds and dense)
+    ("wan720p_sweep", "dynsparse_recall", 0.90, 3, 3),
+    ("wan720p_sweep", "dynsparse_recall", 0.95, 3, 3),
+    ("wan720p_sweep", "dynsparse_recall", 0.98, 3, 3),
+    ("wan720p_sweep", "dynsparse_recall", 0.99, 3, 3),
+    ("wan720p_sweep", "blasst", 1e-2, 3, 3),
+    ("wan720p_sweep", "blasst", 1e-3, 3, 3),
+    ("wan720p_sweep", "blasst", 1e-4, 3, 3),
+    ("wan720p_sweep", "dense", 0.0, 3, 3),
+    ("wan720p_sweep", "dynsparse_lambda", -8.0, 3, 3),
+    ("stress", "dynsparse_recall", 0.95, 4, 4),
+    ("stress", "dynsparse_lambda", -6.0, 4, 4),
+    ("stress", "dynsparse_lambda", -8.0, 4, 4),
+]
 
 
 @pytest.mark.slow
-def test_wan480p_sampled():
-    _full("wan480p", [("dynsparse_recall", 0.95), ("dynsparse_lambda", -8.0)], seed=1)
+@pytest.mark.parametrize("name,rule,param,n_heads,seed", FULL_CASES)
+def test_full_size_sampled(name, rule, param, n_heads, seed):
+    g, tiles = _full(name, rule, param, n_heads=n_heads, seed=seed)
+    if rule == "dynsparse_lambda" and param <= -8.0:
+        # thresholds that skip part of every head: the sample holds mixed runs
+        assert _has_mixed_runs(g, tiles)
 
 
-@pytest.mark.slow
-def test_wan720p_sampled():
-    _full("wan720p", [("dynsparse_recall", 0.95), ("dense", 0.0), ("dynsparse_lambda", -8.0)],
-          seed=2)
-
-
-@pytest.mark.slow
-def test_wan720p_sweep_sampled():
-    _full("wan720p_sweep", [("dynsparse_recall", 0.9), ("dynsparse_recall", 0.99),
-                            ("blasst", 1e-2), ("blasst", 1e-4)], n_heads=3, seed=3)
-
-
-@pytest.mark.slow
-def test_stress_sampled():
-    _full("stress", [("dynsparse_recall", 0.95), ("dynsparse_lambda", -6.0)], n_heads=4,
-          seed=4)
+def test_release_full_size_inputs():
+    _HELD.clear()
 
 
 @pytest.mark.slow
