@@ -240,8 +240,9 @@ size_t dsattn_reordered_workspace_bytes(int B, int H, int N, int d, int with_lse
  * arrays that must be permutations of 0..N-1 (not checked; see dsattn_gather_rows for
  * entries outside [0, N)).  workspace is a caller-owned device buffer of at least
  * dsattn_reordered_workspace_bytes(B, H, N, d, lse_out != NULL) bytes, 256-byte aligned,
- * overlapping none of q, k, v, o; its contents are overwritten.  Everything else as
- * dsattn_attn_fwd_ex.
+ * overlapping no other buffer of the call (q, k, v, o, lse_out, mask_out, stats_out,
+ * mask_in, q_index, kv_index); its contents are overwritten.  q_index and kv_index must
+ * not overlap any output either.  Everything else as dsattn_attn_fwd_ex.
  */
 int dsattn_attn_fwd_reordered(const dsattn_args* args, const int32_t* q_index,
                               const int32_t* kv_index, void* workspace,

@@ -20,7 +20,10 @@ import math
 import os
 
 LIB_NAME = "libdsattn.so"
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), LIB_NAME)
+# DSATTN_LIB selects another build of the same library (for instance the host-sanitizer
+# build, libdsattn_san.so); by default the in-tree libdsattn.so is loaded.
+LIB_PATH = os.environ.get("DSATTN_LIB") or os.path.join(
+    os.path.dirname(os.path.abspath(__file__)), LIB_NAME)
 
 TILE_Q = 128
 TILE_K = 64

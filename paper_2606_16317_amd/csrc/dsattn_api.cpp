@@ -116,32 +116,36 @@ bool overlap(const Span& x, const Span& y) {
   return x.lo < x.hi && y.lo < y.hi && x.lo < y.hi && y.lo < x.hi;
 }
 
-// Every output must be disjoint from every input and from the other outputs (the kernels
-// read inputs while writing outputs, from many workgroups at once).
-int check_overlaps(const dsattn_args& a) {
+// Byte ranges of the buffers one attention call reads (inputs) and writes (outputs).
+struct CallSpans {
+  Span in[6];
+  Span out[4];
+};
+
+CallSpans call_spans(const dsattn_args& a) {
   const size_t rows = (size_t)a.B * (size_t)a.H * (size_t)a.N;
   const bool q8 = a.qk_format == DSATTN_QK_MXFP8;
   const size_t qk_bytes = rows * (size_t)kHeadDim * (q8 ? 1 : 2);
   const size_t units = (size_t)a.B * (size_t)a.H * (size_t)((a.N + a.tile_q - 1) / a.tile_q);
   const size_t mask_bytes = units * (size_t)((a.N + a.tile_k - 1) / a.tile_k);
-  const Span in[] = {
-      span("q", a.q, qk_bytes),
-      span("k", a.k, qk_bytes),
-      span("v", a.v, rows * kHeadDim * 2),
-      span("q_scales", q8 ? a.q_scales : nullptr, rows * 4),
-      span("k_scales", q8 ? a.k_scales : nullptr, rows * 4),
-      span("mask_in", a.rule == DSATTN_RULE_MASK ? a.mask_in : nullptr, mask_bytes),
-  };
-  const Span out[] = {
-      span("o", a.o, rows * kHeadDim * 2),
-      span("lse_out", a.lse_out, rows * 4),
-      span("mask_out", a.mask_out, mask_bytes),
-      span("stats_out", a.stats_out, (size_t)a.B * (size_t)a.H * 4 * sizeof(uint64_t)),
-  };
-  for (const Span& w : out) {
-    for (const Span& r : in)
+  return CallSpans{
+      {span("q", a.q, qk_bytes), span("k", a.k, qk_bytes), span("v", a.v, rows * kHeadDim * 2),
+       span("q_scales", q8 ? a.q_scales : nullptr, rows * 4),
+       span("k_scales", q8 ? a.k_scales : nullptr, rows * 4),
+       span("mask_in", a.rule == DSATTN_RULE_MASK ? a.mask_in : nullptr, mask_bytes)},
+      {span("o", a.o, rows * kHeadDim * 2), span("lse_out", a.lse_out, rows * 4),
+       span("mask_out", a.mask_out, mask_bytes),
+       span("stats_out", a.stats_out, (size_t)a.B * (size_t)a.H * 4 * sizeof(uint64_t))}};
+}
+
+// Every output must be disjoint from every input and from the other outputs (the kernels
+// read inputs while writing outputs, from many workgroups at once).
+int check_overlaps(const dsattn_args& a) {
+  const CallSpans c = call_spans(a);
+  for (const Span& w : c.out) {
+    for (const Span& r : c.in)
       if (overlap(w, r)) return fail(DSATTN_EINVAL, "%s must not overlap %s", w.name, r.name);
-    for (const Span& w2 : out)
+    for (const Span& w2 : c.out)
       if (&w2 < &w && overlap(w, w2))
         return fail(DSATTN_EINVAL, "%s must not overlap %s", w.name, w2.name);
   }
@@ -503,17 +507,26 @@ int dsattn_attn_fwd_reordered(const dsattn_args* args, const int32_t* q_index,
   if (workspace_size < need)
     return fail(DSATTN_EINVAL, "workspace too small: %zu bytes given, %zu needed", workspace_size, need);
 
+  // The gathers read q, k, v and the index arrays into the workspace, the kernel reads
+  // and writes the workspace while writing mask_out and stats_out, and the scatters read
+  // the workspace and q_index into o and lse_out: the workspace must be disjoint from
+  // every argument buffer, and the index arrays from everything written.
+  const CallSpans c = call_spans(a);
+  const Span ws_span = span("workspace", workspace, need);
+  const Span idx[] = {span("q_index", q_index, (size_t)a.N * 4),
+                      span("kv_index", kv_index, (size_t)a.N * 4)};
+  for (const Span& r : c.in)
+    if (overlap(ws_span, r)) return fail(DSATTN_EINVAL, "workspace must not overlap %s", r.name);
+  for (const Span& w : c.out)
+    if (overlap(ws_span, w)) return fail(DSATTN_EINVAL, "workspace must not overlap %s", w.name);
+  for (const Span& i : idx) {
+    if (overlap(ws_span, i)) return fail(DSATTN_EINVAL, "workspace must not overlap %s", i.name);
+    for (const Span& w : c.out)
+      if (overlap(w, i)) return fail(DSATTN_EINVAL, "%s must not overlap %s", w.name, i.name);
+  }
   const int bh = a.B * a.H;
   const size_t slice = round_up((size_t)bh * (size_t)a.N * (size_t)a.d * 2);
   char* ws = static_cast<char*>(workspace);
-  const uintptr_t w0 = reinterpret_cast<uintptr_t>(ws), w1 = w0 + need;
-  const size_t tensor_bytes = (size_t)bh * (size_t)a.N * (size_t)a.d * 2;
-  const void* io[] = {a.q, a.k, a.v, a.o};
-  for (const void* p : io) {
-    const uintptr_t p0 = reinterpret_cast<uintptr_t>(p);
-    if (p0 < w1 && w0 < p0 + tensor_bytes)
-      return fail(DSATTN_EINVAL, "workspace must not overlap q, k, v or o");
-  }
   dsattn_args r = a;  // the same problem over the reordered sequence
   r.q = ws;
   r.k = ws + slice;

@@ -93,3 +93,54 @@ def test_touching_buffers_are_accepted():
                                  to_device(v), scale=SCALE)
     torch.cuda.synchronize()
     assert torch.equal(pool[3 * elems:4 * elems], ref.reshape(-1))
+
+
+def test_reordered_workspace_and_index_overlaps_are_rejected():
+    """The reordered entry point gathers into its workspace, runs the kernel over it and
+    scatters back: a workspace that aliases any other argument buffer, or an index array
+    that aliases an output, is rejected on the host before anything is enqueued."""
+    import torch
+    import paper_2606_16317_amd as dsa
+
+    print("\n[case] reordered overlap checks", flush=True)
+    N, BH = 256, 2
+    elems = BH * N * 128
+    pool = torch.zeros(8 * elems, dtype=torch.bfloat16, device="cuda")
+    base = pool.data_ptr()
+    t = lambda i: base + i * elems * 2
+    q, k, v, o = t(0), t(1), t(2), t(3)
+    need = dsa.dsattn_reordered_workspace_bytes(1, BH, N, 128, with_lse=True)
+    ws = torch.empty(need + 4096, dtype=torch.uint8, device="cuda")
+    w0 = ws.data_ptr()
+    idx = torch.arange(N, dtype=torch.int32, device="cuda")
+    extra = torch.zeros(64 * 1024, dtype=torch.uint8, device="cuda")
+    e0 = extra.data_ptr()
+
+    def run(q_index=idx.data_ptr(), kv_index=idx.data_ptr(), workspace=w0, **kw):
+        a = args_for(dsa, q, k, v, o, N, **kw)
+        rc = dsa.lib().dsattn_attn_fwd_reordered(ctypes.byref(a), ctypes.c_void_p(q_index),
+                                                 ctypes.c_void_p(kv_index),
+                                                 ctypes.c_void_p(workspace),
+                                                 ctypes.c_size_t(need))
+        return rc, dsa.last_error()
+
+    cases = [
+        (dict(lse_out=w0 + 256), "workspace must not overlap lse_out"),
+        (dict(mask_out=w0 + 512), "workspace must not overlap mask_out"),
+        (dict(stats_out=w0 + 1024), "workspace must not overlap stats_out"),
+        (dict(rule=dsa.RULE_MASK, mask_in=w0 + 2048), "workspace must not overlap mask_in"),
+        (dict(q_index=w0 + 4096), "workspace must not overlap q_index"),
+        (dict(kv_index=w0 + 8192), "workspace must not overlap kv_index"),
+        (dict(workspace=o + 256), "workspace must not overlap o"),
+        (dict(q_index=e0, lse_out=e0), "lse_out must not overlap q_index"),
+        (dict(kv_index=e0 + 8, mask_out=e0), "mask_out must not overlap kv_index"),
+        (dict(q_index=e0 + 16, stats_out=e0), "stats_out must not overlap q_index"),
+        (dict(q_index=o + 128), "o must not overlap q_index"),
+    ]
+    for kw, msg in cases:
+        rc, err = run(**kw)
+        assert rc == -1 and msg in err, (kw, rc, err)
+    # disjoint buffers are accepted
+    rc, err = run(lse_out=e0, stats_out=e0 + 32 * 1024)
+    torch.cuda.synchronize()
+    assert rc == 0, err
