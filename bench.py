@@ -2,13 +2,21 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload wan720p]
 
-A step is one call of ``dynsparse_attn_fwd`` (recall target 0.95) over a whole
-Wan-2.2-14B-like 720p attention layer (B=1, H=40, N=75600 = 21x45x80 latent tokens,
-d=128, bf16), with the inputs already resident in HBM.  ``value`` is the effective
-(dense-equivalent) throughput 4*B*H*N^2*d / time; the same run times the library's own
-``dense_attn_fwd`` for the speedup, reports the kernel's bf16 MFMA roofline fraction on
-the work it actually issues, and times the fp64 CPU oracle on a bounded sample of the
-same layer as a reference point.  One JSON line is printed.
+A step is one call of ``dynsparse_attn_fwd`` (recall target 0.95) over one synthetic
+video attention layer -- by default the Wan-2.2-14B-like 720p layer (B=1, H=40,
+N=75600 = 21x45x80 latent tokens, d=128, bf16) -- with the inputs already resident in
+HBM.  ``value`` is the effective (dense-equivalent) throughput 4*B*H*N^2*d / time; the
+same run times the library's own ``dense_attn_fwd`` for the speedup, reports the
+kernel's bf16 MFMA roofline fraction on the work it actually issues and the achieved
+per-row recall (from the kernels' own LSE outputs), and times the fp64 CPU oracle on a
+bounded sample of the same layer, teacher-forced on the GPU's skip mask (which also gives
+the sampled-tile decision mismatch count).  One JSON line is printed.
+
+``--all-configs`` prints one JSON line per workload and rule instead: the tiny, 480p and
+720p layers at their recall target (720p also at the paper's lambda = -6 and at -8),
+every point of the threshold sweep, and the stress layer, each with throughput,
+roofline fraction, speedup over dense, sparsity, relative L2 against dense, achieved
+recall and the oracle mismatch count on sampled query tiles.
 
 ``--sweep`` instead prints one JSON line per rule/threshold on the given workload;
 ``--reorder-sweep`` prints, per rule/threshold, the row-major run next to the same run over
@@ -26,9 +34,12 @@ from __future__ import annotations
 import argparse
 import json
 import math
+import multiprocessing
 import os
 import re
+import shutil
 import sys
+import tempfile
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
@@ -40,6 +51,7 @@ PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 MFMA
 PEAK_FP8_TFLOPS = 5000.0     # MI355X dense fp8 MFMA
 HBM_PEAK_GBS = 8000.0
 TILE_Q, TILE_K, D = 128, 64, 128
+CPU_SHARE = 16               # host cores that go with one GPU on the GPU machines
 
 
 def parse():
@@ -50,8 +62,10 @@ def parse():
     ap.add_argument("--workload", default="wan720p")
     ap.add_argument("--recall", type=float, default=None, help="recall target (default: workload's)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
-                    help="approximate CPU budget of the oracle baseline (0 = skip)")
+                    help="approximate wall-clock budget of the oracle baseline (0 = skip)")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense timing (profiling)")
+    ap.add_argument("--all-configs", action="store_true",
+                    help="one line per workload and rule (throughput, sparsity, error, recall)")
     ap.add_argument("--sweep", action="store_true", help="one line per rule/threshold")
     ap.add_argument("--reorder-sweep", action="store_true",
                     help="row-major vs blocked token order, one line per rule/threshold")
@@ -138,33 +152,477 @@ def gemm_reference(n=8192, steps=10):
     return 2.0 * n ** 3 / (ms * 1e-3) / 1e12
 
 
-def cpu_baseline(q, k, v, scale, lam, budget_s):
-    """Time the fp64 oracle on Q tiles of head (0, 0) for about budget_s seconds."""
+# ---------------------------------------------------------------------------------------
+# CPU leg: the fp64 oracle on the host's cores, one worker process per core with one BLAS
+# thread each.  The pool is started before anything touches the GPU and its workers
+# never do; they read the sampled heads from .npy files (memory-mapped) and run the
+# oracle on their query tiles, teacher-forced on the GPU's skip decisions.
+
+_HEADS = {}
+
+
+_ONE_THREAD = {"OMP_NUM_THREADS": "1", "OPENBLAS_NUM_THREADS": "1", "MKL_NUM_THREADS": "1",
+               "BLIS_NUM_THREADS": "1"}
+
+
+def _worker_init():
+    # one BLAS thread per worker: set before numpy (and its BLAS) is first imported here,
+    # then enforced on whatever BLAS got loaded
+    os.environ.update(_ONE_THREAD)
+    import numpy  # noqa: F401
+
+    try:
+        from threadpoolctl import threadpool_limits
+
+        threadpool_limits(1)
+    except Exception:
+        pass
+
+
+def _oracle_task(task):
+    """Run the oracle on one query tile; returns timing and the comparison with the GPU."""
     import numpy as np
     import oracle
 
-    try:
-        from threadpoolctl import threadpool_info
-
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = 1
-    N = q.shape[2]
-    n_qt = -(-N // TILE_Q)
+    path, hi, qi, rule, thr, forced, o_gpu = task
+    if path not in _HEADS:
+        _HEADS.clear()
+        _HEADS[path] = tuple(np.load(os.path.join(path, f"{x}.npy"), mmap_mode="r")
+                             for x in ("q", "k", "v"))
+    q, k, v = _HEADS[path]
     t0 = time.perf_counter()
-    oracle.rule_attention(q, k, v, scale, "dynsparse", lam, TILE_Q, TILE_K, tiles=[(0, 0, 0)])
-    per_tile = time.perf_counter() - t0
-    n = int(max(1, min(n_qt, budget_s / max(per_tile, 1e-3))))
-    picks = sorted(set(np.linspace(0, n_qt - 1, n).astype(int).tolist()))
-    tiles = [(0, 0, i) for i in picks]
-    t0 = time.perf_counter()
-    oracle.rule_attention(q, k, v, scale, "dynsparse", lam, TILE_Q, TILE_K, tiles=tiles)
+    run = oracle.rule_attention(q[hi:hi + 1][None], k[hi:hi + 1][None], v[hi:hi + 1][None],
+                                1.0 / math.sqrt(D), rule, thr, TILE_Q, TILE_K,
+                                tiles=[(0, 0, qi)], forced_mask=forced)
     dt = time.perf_counter() - t0
-    rows = sum(min(N, (i + 1) * TILE_Q) - i * TILE_Q for i in picks)
-    eff = 4.0 * rows * N * D / dt / 1e12
-    return {"value": eff, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{len(tiles)} of {n_qt} query tiles of head (0,0), all {-(-N // TILE_K)} "
-                      f"key tiles each, {dt:.1f} s; dense-equivalent FLOP of the sample / time"}
+    res = run.results[0]
+    r0, r1 = run.row_ranges[0]
+    own = res.margin < 0
+    bad = own != res.skip
+    worst = float(np.abs(res.margin[bad]).max()) if bad.any() else 0.0
+    err = 0.0
+    if o_gpu is not None:
+        err = float(np.abs(oracle.bf16_to_f64(o_gpu) - res.o_sparse).max())
+    return {"seconds": dt, "rows": r1 - r0, "mismatches": int(bad.sum()), "worst": worst,
+            "near": int((np.abs(res.margin) < 1e-3).sum()), "o_max_abs": err}
+
+
+def host_cpu():
+    """CPU model, visible logical CPUs and the physical cores behind them."""
+    cpus = sorted(os.sched_getaffinity(0))
+    model, phys = "unknown", set()
+    try:
+        cur = {}
+        for line in open("/proc/cpuinfo"):
+            if not line.strip():
+                if cur.get("processor") is not None and int(cur["processor"]) in cpus:
+                    phys.add((cur.get("physical id"), cur.get("core id")))
+                    model = cur.get("model name", model)
+                cur = {}
+                continue
+            key, _, val = line.partition(":")
+            cur[key.strip()] = val.strip()
+    except OSError:
+        pass
+    return {"cpu_model": model, "logical_cpus_visible": len(cpus),
+            "physical_cores_visible": len(phys) or None}
+
+
+class OracleLeg:
+    """Spawned worker pool for the oracle; created before the first GPU call."""
+
+    def __init__(self):
+        self.info = host_cpu()
+        self.workers = max(1, min(self.info["logical_cpus_visible"],
+                                  int(os.environ.get("OMP_NUM_THREADS", CPU_SHARE)), CPU_SHARE))
+        ctx = multiprocessing.get_context("spawn")
+        saved = {k: os.environ.get(k) for k in _ONE_THREAD}
+        os.environ.update(_ONE_THREAD)          # inherited by the spawned workers
+        try:
+            self.pool = ctx.Pool(self.workers, initializer=_worker_init)
+        finally:
+            for k, val in saved.items():
+                if val is None:
+                    os.environ.pop(k, None)
+                else:
+                    os.environ[k] = val
+        self.dir = tempfile.mkdtemp(prefix="dsattn_oracle_")
+        self.paths = {}
+
+    def stage(self, name, q, k, v, heads):
+        """Write the sampled heads (list of flat b*H + h indices) of one workload."""
+        import numpy as np
+
+        path = os.path.join(self.dir, name)
+        os.makedirs(path, exist_ok=True)
+        B, H = q.shape[:2]
+        for x, arr in (("q", q), ("k", k), ("v", v)):
+            np.save(os.path.join(path, f"{x}.npy"), arr.reshape(B * H, *arr.shape[2:])[heads])
+        self.paths[name] = (path, list(heads))
+
+    def run(self, name, rule, thr, tiles, mask=None, o=None, budget_s=None):
+        """Oracle over ``tiles`` = [(flat head, query tile)], teacher-forced on ``mask``
+        ([BH][n_qt][n_kt] numpy, or None).  With budget_s the sample is cut to what the
+        pool does in about that long (from the time of a first round of one tile per
+        worker)."""
+        path, heads = self.paths[name]
+        pos = {h: i for i, h in enumerate(heads)}
+
+        def task(t):
+            bh, qi = t
+            f = None if mask is None else mask[bh][None, None]
+            og = None if o is None else o[bh, qi * TILE_Q:(qi + 1) * TILE_Q]
+            return (path, pos[bh], qi, rule, thr, f, og)
+
+        tiles = list(tiles)
+        t0 = time.perf_counter()
+        # generous deadlines: a worker that cannot start must not hang the bench
+        first = self.pool.map_async(_oracle_task, [task(t) for t in tiles[:self.workers]]
+                                    ).get(timeout=600)
+        done = list(first)
+        rest = tiles[self.workers:]
+        if budget_s is not None and rest:
+            per_round = time.perf_counter() - t0
+            rounds = max(0, int(budget_s / max(per_round, 1e-3)) - 1)
+            rest = rest[:rounds * self.workers]
+        if rest:
+            done += self.pool.map_async(_oracle_task, [task(t) for t in rest], chunksize=1
+                                        ).get(timeout=600 + 4 * (budget_s or 600))
+        wall = time.perf_counter() - t0
+        n = len(done)
+        return {"tiles": n, "wall_s": wall, "rows": sum(r["rows"] for r in done),
+                "mismatches": sum(r["mismatches"] for r in done),
+                "max_mismatch_margin": max([r["worst"] for r in done] or [0.0]),
+                "within_band": sum(r["near"] for r in done),
+                "o_max_abs_vs_gpu": max([r["o_max_abs"] for r in done] or [0.0]),
+                "sampled": tiles[:n]}
+
+    def close(self):
+        self.pool.close()
+        self.pool.join()
+        shutil.rmtree(self.dir, ignore_errors=True)
+
+
+def spread_tiles(heads, n_qt, per_head):
+    """Query tiles spread evenly over each head (always the first and the last)."""
+    import numpy as np
+
+    picks = sorted(set(np.linspace(0, n_qt - 1, max(2, per_head)).round().astype(int).tolist()))
+    # interleave heads so that a cut sample still covers every head
+    return [(h, qi) for qi in picks for h in heads]
+
+
+def cpu_baseline_record(res, N, workers, info, name, forced=True):
+    eff = 4.0 * res["rows"] * N * D / res["wall_s"] / 1e12
+    how = "teacher-forced on the GPU mask" if forced else "own decisions"
+    return {"value": eff, "unit": "TFLOP/s", "cores": workers, "kind": "oracle",
+            "sample": f"{res['tiles']} query tiles of {name} spread over sampled heads, every "
+                      f"key tile of each, {how}; "
+                      f"{res['wall_s']:.1f} s wall on {workers} worker processes with one "
+                      f"BLAS thread each; dense-equivalent FLOP of the sample / wall time",
+            "cpu_model": info["cpu_model"], "physical_cores_visible": info["physical_cores_visible"],
+            "logical_cpus_visible": info["logical_cpus_visible"], "blas_threads_per_worker": 1}
+
+
+# ---------------------------------------------------------------------------------------
+# GPU measurement of one rule on one workload
+
+def rule_ids(dsa):
+    return {"dense": dsa.RULE_DENSE, "dynsparse_recall": dsa.RULE_DYNSPARSE_RECALL,
+            "dynsparse_lambda": dsa.RULE_DYNSPARSE_LAMBDA, "blasst": dsa.RULE_BLASST}
+
+
+def oracle_threshold(rule, p, N):
+    if rule == "dense":
+        return "dense", 0.0
+    if rule == "blasst":
+        return "blasst", math.log(p) if p > 0 else -math.inf
+    if rule == "dynsparse_recall":
+        return "dynsparse", math.log((1.0 - p) / N) if p < 1 else -math.inf
+    return "dynsparse", p
+
+
+class Layer:
+    """Device copies of one workload plus its dense reference (time, output, LSE)."""
+
+    def __init__(self, dsa, w, q, k, v, steps, warmup, dense=True):
+        import torch
+
+        self.dsa, self.w = dsa, w
+        self.B, self.H, self.N = w.B, w.H, w.N
+        self.qd, self.kd, self.vd = upload(q), upload(k), upload(v)
+        self.o = torch.empty_like(self.qd)
+        self.od = torch.empty_like(self.qd)
+        self.stats = torch.zeros(self.B * self.H * 4, dtype=torch.int64, device="cuda")
+        self.lse = torch.empty(self.B * self.H * self.N, dtype=torch.float32, device="cuda")
+        self.lse_d = torch.empty_like(self.lse)
+        self.dense_flop = 4.0 * self.B * self.H * self.N * self.N * D
+        self.steps, self.warmup = steps, warmup
+        self.dense_ms = None
+        if dense:
+            self.dense_ms = time_calls(lambda: dsa.dense_attn_fwd(self.qd, self.kd, self.vd,
+                                                                  self.od, scale=self.scale),
+                                       steps, warmup)
+            dsa.dsattn_attn_fwd_ex(dsa.RULE_DENSE, 0.0, self.qd, self.kd, self.vd, self.od,
+                                   scale=self.scale, lse_out=self.lse_d)
+
+    @property
+    def scale(self):
+        return 1.0 / math.sqrt(D)
+
+    def measure(self, rule, p, tile_q=TILE_Q, tile_k=TILE_K, mask=None, time_it=True):
+        """Time the rule (unless time_it is False), then, outside the timed region, one call
+        with its LSE and mask for recall, relative L2 against dense, and the decisions."""
+        import torch
+
+        dsa = self.dsa
+        rid = rule_ids(dsa)[rule]
+        fn = lambda: dsa.dsattn_attn_fwd_ex(rid, p, self.qd, self.kd, self.vd, self.o,
+                                            scale=self.scale, tile_q=tile_q, tile_k=tile_k,
+                                            stats_out=self.stats)
+        rec = {}
+        if time_it:
+            ms = time_calls(fn, self.steps, self.warmup)
+            st = self.stats.cpu().numpy().reshape(self.B * self.H, 4)
+            flop = algorithmic_flops(st)
+            rec = {"ms": ms, "effective_tflops": self.dense_flop / (ms * 1e-3) / 1e12,
+                   "actual_tflops": flop / (ms * 1e-3) / 1e12,
+                   "roofline_frac": flop / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+                   "sparsity_tiles": float(st[:, 1].sum() / st[:, 0].sum()),
+                   "sparsity_elems": float(st[:, 3].sum() / st[:, 2].sum())}
+        dsa.dsattn_attn_fwd_ex(rid, p, self.qd, self.kd, self.vd, self.o, scale=self.scale,
+                               tile_q=tile_q, tile_k=tile_k, lse_out=self.lse, mask_out=mask)
+        torch.cuda.synchronize()
+        if time_it and self.dense_ms is not None:
+            rec["dense_ms"] = self.dense_ms
+            rec["speedup_vs_dense"] = self.dense_ms / ms
+        if self.dense_ms is not None:
+            od, o = self.od.float(), self.o.float()
+            rec["rel_l2_vs_dense"] = float((o - od).pow(2).sum().sqrt() / od.pow(2).sum().sqrt())
+            # per-row recall: dense softmax mass of the kept keys, exp(LSE_kept - LSE_all)
+            r = torch.exp(self.lse.double() - self.lse_d.double())
+            rec["recall_min"] = float(r.min())
+            rec["recall_mean"] = float(r.mean())
+        return rec
+
+
+def layer_inputs(w):
+    from synth import workload_inputs
+
+    return workload_inputs(w)
+
+
+def sample_heads(w, n):
+    import numpy as np
+
+    BH = w.B * w.H
+    return sorted(set(np.linspace(0, BH - 1, min(n, BH)).round().astype(int).tolist()))
+
+
+def main():
+    args = parse()
+    if args.trace_summary:
+        print(trace_summary(args.trace_summary, args.command))
+        return
+    if args.traffic_summary:
+        rec = traffic_summary(*args.traffic_summary, args.workload, args.command)
+        path = os.path.join(ROOT, "profiles", f"hbm_traffic_{args.workload}.json")
+        with open(path, "w") as fh:
+            json.dump(rec, fh, indent=1)
+        print(json.dumps(rec))
+        return
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(--gpus must be 1)", file=sys.stderr)
+        sys.exit(2)
+
+    from synth import WORKLOADS
+
+    sweeps = args.sweep or args.reorder_sweep or args.reuse_sweep or args.q8_sweep
+    # The oracle's worker pool starts before the first GPU call.
+    leg = OracleLeg() if (args.cpu_seconds > 0 and not sweeps) else None
+    try:
+        if args.all_configs:
+            return all_configs(args, leg)
+        w = WORKLOADS[args.workload]
+        print(f"[bench] generating {w.describe()}", file=sys.stderr, flush=True)
+        q, k, v, meta = layer_inputs(w)
+        if leg is not None:
+            leg.stage(w.name, q, k, v, sample_heads(w, 8))
+        import torch  # noqa: F401  (first GPU use below)
+
+        import paper_2606_16317_amd as dsa
+
+        if sweeps:
+            return legacy_sweeps(args, dsa, w, q, k, v)
+        return headline(args, dsa, w, q, k, v, leg)
+    finally:
+        if leg is not None:
+            leg.close()
+
+
+def headline(args, dsa, w, q, k, v, leg):
+    import torch
+
+    recall = w.recall if args.recall is None else args.recall
+    B, H, N = w.B, w.H, w.N
+    lam = dsa.dsattn_lambda_from_recall(recall, N)
+    L = Layer(dsa, w, q, k, v, args.steps, args.warmup, dense=not args.no_dense)
+    n_qt, n_kt = -(-N // TILE_Q), -(-N // TILE_K)
+    mask = torch.empty(B * H * n_qt * n_kt, dtype=torch.uint8, device="cuda")
+    print(f"[bench] dynsparse recall={recall} lambda={lam:.3f}: {args.warmup} warmup + "
+          f"{args.steps} timed steps", file=sys.stderr, flush=True)
+
+    # the timed step: dynsparse_attn_fwd (named entry point) with stats
+    def step():
+        dsa.dynsparse_attn_fwd(L.qd, L.kd, L.vd, L.o, scale=L.scale, recall_target=recall,
+                               stats_out=L.stats)
+
+    ms = time_calls(step, args.steps, args.warmup)
+    st = L.stats.cpu().numpy().reshape(B * H, 4)
+    flop_alg = algorithmic_flops(st)
+    achieved = flop_alg / (ms * 1e-3) / 1e12
+    # outside the timed region: LSE, mask and output of the same rule for recall, error
+    # and the oracle comparison
+    rec = L.measure("dynsparse_recall", recall, mask=mask, time_it=False)
+
+    traffic = measured_traffic(w.name)
+    if args.calib_copy:
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
+    gemm = None if args.no_gemm_ref else gemm_reference()
+    cpu, oracle_cmp = None, None
+    if leg is not None:
+        print("[bench] cpu oracle baseline (teacher-forced on the GPU mask)", file=sys.stderr,
+              flush=True)
+        m = mask.cpu().numpy().reshape(B * H, n_qt, n_kt)
+        o_np = L.o.view(torch.int16).cpu().numpy().view("uint16").reshape(B * H, N, D)
+        _, heads = leg.paths[w.name]
+        name, thr = oracle_threshold("dynsparse_recall", recall, N)
+        res = leg.run(w.name, name, thr, spread_tiles(heads, n_qt, 64), mask=m, o=o_np,
+                      budget_s=args.cpu_seconds)
+        cpu = cpu_baseline_record(res, N, leg.workers, leg.info, w.name)
+        oracle_cmp = {k_: res[k_] for k_ in ("tiles", "mismatches", "max_mismatch_margin",
+                                            "within_band", "o_max_abs_vs_gpu")}
+
+    dense_ms = L.dense_ms
+    out = {
+        "metric": METRIC,
+        "value": L.dense_flop / (ms * 1e-3) / 1e12,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{w.describe()}; bf16 in / fp32 accumulate, "
+                               f"tile {TILE_Q}x{TILE_K}",
+                   "rule": "dynsparse", "recall_target": recall, "lambda": lam,
+                   "seed": w.seed},
+        "speedup_vs_dense": (dense_ms / ms) if dense_ms else None,
+        "dense_ms_per_step": dense_ms,
+        "dense_effective_tflops": (L.dense_flop / (dense_ms * 1e-3) / 1e12) if dense_ms else None,
+        "actual_tflops": achieved,
+        "sparsity_tiles": float(st[:, 1].sum() / st[:, 0].sum()),
+        "sparsity_elems": float(st[:, 3].sum() / st[:, 2].sum()),
+        "rel_l2_vs_dense": rec.get("rel_l2_vs_dense"),
+        "recall_min": rec.get("recall_min"),
+        "recall_mean": rec.get("recall_mean"),
+        "oracle_comparison": oracle_cmp,
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
+                     "traffic": traffic},
+        "cpu_baseline": cpu,
+        "context": {"hipblaslt_bf16_gemm_tflops": gemm,
+                    "note": "torch.matmul 8192^3 bf16 on the same GPU: the dense MFMA rate a "
+                            "tuned library sustains here, next to the 2500 TFLOP/s headline"},
+    }
+    print(json.dumps(out), flush=True)
+
+
+# the per-config record: (workload, rule, parameter) in the order printed
+ALL_CONFIGS = [("tiny", "dynsparse_recall", 0.95),
+               ("wan480p", "dynsparse_recall", 0.95),
+               ("wan720p", "dynsparse_recall", 0.95),
+               ("wan720p", "dynsparse_lambda", -8.0),
+               ("wan720p", "dynsparse_lambda", -6.0),
+               ("wan720p_sweep", "dynsparse_recall", 0.90),
+               ("wan720p_sweep", "dynsparse_recall", 0.95),
+               ("wan720p_sweep", "dynsparse_recall", 0.98),
+               ("wan720p_sweep", "dynsparse_recall", 0.99),
+               ("wan720p_sweep", "blasst", 1e-2),
+               ("wan720p_sweep", "blasst", 1e-3),
+               ("wan720p_sweep", "blasst", 1e-4),
+               ("wan720p_sweep", "dense", 0.0),
+               ("stress", "dynsparse_recall", 0.95),
+               ("stress", "dynsparse_lambda", -6.0)]
+
+
+def all_configs(args, leg):
+    import torch
+
+    from synth import WORKLOADS
+
+    current = None
+    for name, rule, p in ALL_CONFIGS:
+        w = WORKLOADS[name]
+        if current is None or current[0] != name:
+            current = None
+            print(f"[all-configs] generating {w.describe()}", file=sys.stderr, flush=True)
+            q, k, v, meta = layer_inputs(w)
+            if leg is not None:
+                leg.stage(name, q, k, v, sample_heads(w, 4))
+            import paper_2606_16317_amd as dsa
+
+            # tiny layers need more calls per timing to rise above launch overhead
+            steps = args.steps * (20 if w.N < 8192 else 1)
+            current = (name, Layer(dsa, w, q, k, v, steps, args.warmup))
+            del q, k, v
+        L = current[1]
+        n_qt, n_kt = -(-w.N // TILE_Q), -(-w.N // TILE_K)
+        mask = torch.empty(w.B * w.H * n_qt * n_kt, dtype=torch.uint8, device="cuda")
+        print(f"[all-configs] {name} {rule} {p}", file=sys.stderr, flush=True)
+        rec = L.measure(rule, p, mask=mask)
+        name_o, thr = oracle_threshold(rule, p, w.N)
+        out = {"workload": w.describe(), "rule": rule, "param": p,
+               "threshold_natural_log": thr if rule != "dense" else None,
+               "tile_q": TILE_Q, "tile_k": TILE_K, **rec}
+        if leg is not None:
+            m = mask.cpu().numpy().reshape(w.B * w.H, n_qt, n_kt)
+            o_np = L.o.view(torch.int16).cpu().numpy().view("uint16").reshape(w.B * w.H, w.N, D)
+            _, heads = leg.paths[name]
+            res = leg.run(name, name_o, thr, spread_tiles(heads, n_qt, 4), mask=m, o=o_np)
+            out["oracle_sampled"] = {k_: res[k_] for k_ in ("tiles", "mismatches",
+                                                           "max_mismatch_margin", "within_band",
+                                                           "o_max_abs_vs_gpu", "wall_s")}
+        print(json.dumps(out), flush=True)
+    current = None
+
+
+def legacy_sweeps(args, dsa, w, q, k, v):
+    import torch
+
+    B, H, N = w.B, w.H, w.N
+    scale = 1.0 / math.sqrt(D)
+    qd, kd, vd = upload(q), upload(k), upload(v)
+    o = torch.empty_like(qd)
+    od = torch.empty_like(qd)
+    stats = torch.zeros(B * H * 4, dtype=torch.int64, device="cuda")
+    dense_flop = 4.0 * B * H * N * N * D
+    if args.sweep:
+        return sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop)
+    if args.reorder_sweep:
+        return reorder_sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop)
+    if args.reuse_sweep:
+        return reuse_sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop)
+    return q8_sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop)
 
 
 def _find_csv(d, suffix):
@@ -222,127 +680,6 @@ def traffic_summary(fetch_dir, write_dir, workload, command):
            "dispatches": [len(f["main"]), len(w["main"])], "command": command,
            "kernel_sha256": kernel_source_digest()}
     return rec
-
-
-def main():
-    args = parse()
-    if args.trace_summary:
-        print(trace_summary(args.trace_summary, args.command))
-        return
-    if args.traffic_summary:
-        rec = traffic_summary(*args.traffic_summary, args.workload, args.command)
-        path = os.path.join(ROOT, "profiles", f"hbm_traffic_{args.workload}.json")
-        with open(path, "w") as fh:
-            json.dump(rec, fh, indent=1)
-        print(json.dumps(rec))
-        return
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
-              "(--gpus must be 1)", file=sys.stderr)
-        sys.exit(2)
-
-    import numpy as np
-    import torch
-
-    import paper_2606_16317_amd as dsa
-    from synth import WORKLOADS, workload_inputs
-
-    w = WORKLOADS[args.workload]
-    recall = w.recall if args.recall is None else args.recall
-    B, H, N = w.B, w.H, w.N
-    scale = 1.0 / math.sqrt(D)
-    print(f"[bench] generating {w.describe()}", file=sys.stderr, flush=True)
-    q, k, v, meta = workload_inputs(w)
-    qd, kd, vd = upload(q), upload(k), upload(v)
-    o = torch.empty_like(qd)
-    od = torch.empty_like(qd)
-    stats = torch.zeros(B * H * 4, dtype=torch.int64, device="cuda")
-    dense_stats = torch.zeros(B * H * 4, dtype=torch.int64, device="cuda")
-    dense_flop = 4.0 * B * H * N * N * D
-    lam = dsa.dsattn_lambda_from_recall(recall, N)
-
-    if args.sweep:
-        return sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop)
-    if args.reorder_sweep:
-        return reorder_sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop)
-    if args.reuse_sweep:
-        return reuse_sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop)
-    if args.q8_sweep:
-        return q8_sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop)
-
-    def step():
-        dsa.dynsparse_attn_fwd(qd, kd, vd, o, scale=scale, recall_target=recall, stats_out=stats)
-
-    print(f"[bench] dynsparse recall={recall} lambda={lam:.3f}: {args.warmup} warmup + "
-          f"{args.steps} timed steps", file=sys.stderr, flush=True)
-    ms = time_calls(step, args.steps, args.warmup)
-    st = stats.cpu().numpy().reshape(B * H, 4)
-    flop_alg = algorithmic_flops(st)
-    sp_tiles = float(st[:, 1].sum() / st[:, 0].sum())
-    sp_elems = float(st[:, 3].sum() / st[:, 2].sum())
-
-    dense_ms = None
-    rel_l2 = None
-    if not args.no_dense:
-        print("[bench] dense reference timing", file=sys.stderr, flush=True)
-
-        def dstep():
-            dsa.dense_attn_fwd(qd, kd, vd, od, scale=scale, stats_out=dense_stats)
-
-        dense_ms = time_calls(dstep, args.steps, args.warmup)
-        diff = (o.float() - od.float()).pow(2).sum().sqrt()
-        rel_l2 = float(diff / od.float().pow(2).sum().sqrt())
-
-    achieved = flop_alg / (ms * 1e-3) / 1e12
-    traffic = measured_traffic(w.name)
-    if args.calib_copy:
-        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
-        dst = torch.empty_like(src)
-        torch.mul(src, 1.0, out=dst)
-        torch.cuda.synchronize()
-        del src, dst
-    gemm = None
-    if not args.no_gemm_ref:
-        gemm = gemm_reference()
-    cpu = None
-    if args.cpu_seconds > 0:
-        print("[bench] cpu oracle baseline", file=sys.stderr, flush=True)
-        cpu = cpu_baseline(q, k, v, scale, lam, args.cpu_seconds)
-
-    out = {
-        "metric": METRIC,
-        "value": dense_flop / (ms * 1e-3) / 1e12,
-        "unit": "TFLOP/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": ms,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic",
-        "config": {"workload": f"{w.name}: Wan-2.2-14B-like 720p attention layer, "
-                               f"B={B} H={H} N={N} ({'x'.join(map(str, w.grid))}) d={D}, "
-                               f"bf16 in / fp32 accumulate, tile {TILE_Q}x{TILE_K}",
-                   "rule": "dynsparse", "recall_target": recall, "lambda": lam,
-                   "seed": w.seed},
-        "speedup_vs_dense": (dense_ms / ms) if dense_ms else None,
-        "dense_ms_per_step": dense_ms,
-        "dense_effective_tflops": (dense_flop / (dense_ms * 1e-3) / 1e12) if dense_ms else None,
-        "actual_tflops": achieved,
-        "sparsity_tiles": sp_tiles,
-        "sparsity_elems": sp_elems,
-        "rel_l2_vs_dense": rel_l2,
-        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
-                     "traffic": traffic},
-        "cpu_baseline": cpu,
-        "context": {"hipblaslt_bf16_gemm_tflops": gemm,
-                    "note": "torch.matmul 8192^3 bf16 on the same GPU: the dense MFMA rate a "
-                            "tuned library sustains here, next to the 2500 TFLOP/s headline"},
-    }
-    print(json.dumps(out), flush=True)
 
 
 def sweep(args, dsa, w, qd, kd, vd, o, od, stats, scale, dense_flop):
