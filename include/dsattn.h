@@ -249,6 +249,23 @@ int dsattn_attn_fwd_reordered(const dsattn_args* args, const int32_t* q_index,
                               size_t workspace_bytes);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): dsattn_attn_fwd_reordered with its
+ * workspace taken from a scratch array inside the library, so the call allocates
+ * nothing.  Each GPU the library runs on holds one such array of
+ * DSATTN_STATIC_SCRATCH_BYTES until the process ends; a problem whose workspace
+ * (dsattn_reordered_workspace_bytes) exceeds it is rejected with DSATTN_EINVAL.  Every
+ * call on one GPU uses that GPU's array: calls that overlap in time on one GPU (other
+ * streams, other threads) race and give undefined results; calls ordered on one stream
+ * are safe.  The array keeps the last call's contents (nothing in it needs clearing: every
+ * byte a call reads there it has written first).  Everything else as
+ * dsattn_attn_fwd_reordered.
+ */
+#define DSATTN_STATIC_SCRATCH_BYTES ((size_t)96 << 20)
+int dsattn_attn_fwd_reordered_noalloc(const dsattn_args* args, const int32_t* q_index,
+                                      const int32_t* kv_index);
+
+/*
  * MX-FP8 quantisation of bf16 rows, the storage of the quantised Q K^T variant (the
  * Conclusion, Section 5, lists quantisation among the methods the rule combines with).  src holds `rows`
  * rows of `row_len` bf16 values (row_len a multiple of 32); every 32 consecutive values

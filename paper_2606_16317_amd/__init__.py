@@ -110,6 +110,9 @@ def lib():
                                                 ctypes.c_void_p, ctypes.c_void_p,
                                                 ctypes.c_size_t]
         L.dsattn_attn_fwd_reordered.restype = ctypes.c_int
+        L.dsattn_attn_fwd_reordered_noalloc.argtypes = [ctypes.POINTER(DsAttnArgs),
+                                                        ctypes.c_void_p, ctypes.c_void_p]
+        L.dsattn_attn_fwd_reordered_noalloc.restype = ctypes.c_int
         L.dsattn_quantize_mxfp8.argtypes = [ctypes.c_void_p] * 3 + [ctypes.c_longlong,
                                                                       ctypes.c_int,
                                                                       ctypes.c_void_p]
@@ -426,11 +429,39 @@ def dsattn_attn_fwd_reordered(rule, param, q, k, v, q_index, kv_index, o=None, s
     return o
 
 
+STATIC_SCRATCH_BYTES = 96 << 20    # DSATTN_STATIC_SCRATCH_BYTES of include/dsattn.h
+
+
+def dsattn_attn_fwd_reordered_noalloc(rule, param, q, k, v, q_index, kv_index, o=None,
+                                      scale=None, tile_q=TILE_Q, tile_k=TILE_K, stats_out=None,
+                                      mask_out=None, lse_out=None, stream=None,
+                                      key_order=ORDER_ASCENDING):
+    """``dsattn_attn_fwd_reordered`` with the workspace taken from the library's static
+    per-GPU scratch (at most STATIC_SCRATCH_BYTES): the C call allocates nothing.  Pass
+    ``o`` (and any optional outputs) to keep this wrapper from allocating either."""
+    import torch
+
+    o = _out(q, o)
+    B, H, N, d = _shape(q, k, v, o)
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    st, mk, ls = _buffers(B, H, N, stats_out, mask_out, lse_out, tile_q, tile_k)
+    for name, t in (("q_index", q_index), ("kv_index", kv_index)):
+        if t.dtype != torch.int32 or not t.is_cuda or not t.is_contiguous() or t.numel() != N:
+            raise ValueError(f"{name} must be a contiguous int32 GPU tensor of N={N} entries")
+    a = DsAttnArgs(rule, param, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                   B, H, N, d, scale, tile_q, tile_k, _stream(stream), st, mk, ls, key_order)
+    rc = lib().dsattn_attn_fwd_reordered_noalloc(ctypes.byref(a), q_index.data_ptr(),
+                                                 kv_index.data_ptr())
+    _check(rc, "dsattn_attn_fwd_reordered_noalloc")
+    return o
+
+
 __all__ = [
     "HEAD_DIM", "TILE_Q", "TILE_K", "ORDER_ASCENDING", "ORDER_DIAGONAL", "RULE_DENSE", "RULE_BLASST", "RULE_DYNSPARSE_RECALL",
     "RULE_DYNSPARSE_LAMBDA", "RULE_MASK", "DsAttnArgs", "lib", "last_error", "dsattn_lambda_from_recall",
     "dynsparse_attn_fwd", "dynsparse_attn_fwd_lambda", "blasst_attn_fwd", "dense_attn_fwd",
     "dsattn_attn_fwd_ex", "dsattn_block_order", "dsattn_gather_rows", "dsattn_scatter_rows",
-    "dsattn_reordered_workspace_bytes", "dsattn_attn_fwd_reordered", "dsattn_quantize_mxfp8",
+    "dsattn_reordered_workspace_bytes", "dsattn_attn_fwd_reordered",
+    "dsattn_attn_fwd_reordered_noalloc", "STATIC_SCRATCH_BYTES", "dsattn_quantize_mxfp8",
     "dsattn_attn_fwd_mxfp8", "dsattn_key_mean", "QK_BF16", "QK_MXFP8",
 ]

@@ -3,12 +3,13 @@
 
 #include "dsattn.h"
 
-#include <hip/hip_runtime_api.h>
+#include <hip/hip_runtime.h>
 
 #include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <string>
 
 #include "fa_fwd_launch.h"
@@ -480,9 +481,15 @@ size_t dsattn_reordered_workspace_bytes(int B, int H, int N, int d, int with_lse
   return workspace_bytes(B, H, N, d, with_lse != 0);
 }
 
-int dsattn_attn_fwd_reordered(const dsattn_args* args, const int32_t* q_index,
-                              const int32_t* kv_index, void* workspace,
-                              size_t workspace_size) {
+}  // extern "C"
+
+namespace {
+
+// Reordered attention over a workspace of workspace_size bytes.  static_ws: the workspace
+// is the library's own static scratch (device memory by construction; its size is the
+// fixed maximum).
+int reordered(const dsattn_args* args, const int32_t* q_index, const int32_t* kv_index,
+              void* workspace, size_t workspace_size, bool static_ws) {
   if (args == nullptr) return fail(DSATTN_EINVAL, "args must be non-null");
   const dsattn_args& a = *args;
   Request rq;
@@ -499,13 +506,20 @@ int dsattn_attn_fwd_reordered(const dsattn_args* args, const int32_t* q_index,
     return fail(DSATTN_EINVAL, "q_index and kv_index must be device pointers");
   if (!aligned(q_index, 4) || !aligned(kv_index, 4))
     return fail(DSATTN_EINVAL, "q_index and kv_index must be 4-byte aligned");
-  if (!is_device_pointer(workspace)) return fail(DSATTN_EINVAL, "workspace is not a device pointer");
+  if (!static_ws && !is_device_pointer(workspace))
+    return fail(DSATTN_EINVAL, "workspace is not a device pointer");
   if (!aligned(workspace, kSliceAlign))
     return fail(DSATTN_EINVAL, "workspace must be %zu-byte aligned", kSliceAlign);
   const bool with_lse = a.lse_out != nullptr;
   const size_t need = workspace_bytes(a.B, a.H, a.N, a.d, with_lse);
-  if (workspace_size < need)
+  if (workspace_size < need) {
+    if (static_ws)
+      return fail(DSATTN_EINVAL,
+                  "problem too large for the static scratch: %zu bytes needed, %zu available "
+                  "(use dsattn_attn_fwd_reordered with a caller workspace)",
+                  need, workspace_size);
     return fail(DSATTN_EINVAL, "workspace too small: %zu bytes given, %zu needed", workspace_size, need);
+  }
 
   // The gathers read q, k, v and the index arrays into the workspace, the kernel reads
   // and writes the workspace while writing mask_out and stats_out, and the scatters read
@@ -551,6 +565,58 @@ int dsattn_attn_fwd_reordered(const dsattn_args* args, const int32_t* q_index,
   if (e != hipSuccess) return fail(DSATTN_ELAUNCH, "scatter launch failed: %s", hipGetErrorString(e));
   g_last_error.clear();
   return DSATTN_OK;
+}
+
+// Scratch of the allocation-free reordered entry point: one copy per GPU, held until the
+// process ends.  Host code never names the array itself (on the host its name is only a
+// stand-in); it uses the device address hipGetSymbolAddress returns for the current
+// device, looked up once per device on the first call there.
+constexpr size_t kStaticScratchBytes = DSATTN_STATIC_SCRATCH_BYTES;
+constexpr int kMaxDevices = 64;
+static __device__ __attribute__((aligned(256))) unsigned char scratch[kStaticScratchBytes];
+
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int static_scratch(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return fail(DSATTN_EINVAL, "no usable current HIP device");
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr)
+      return fail(DSATTN_ELAUNCH, "static scratch lookup failed on device %d: %s", dev,
+                  hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return DSATTN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int dsattn_attn_fwd_reordered(const dsattn_args* args, const int32_t* q_index,
+                              const int32_t* kv_index, void* workspace,
+                              size_t workspace_size) {
+  return reordered(args, q_index, kv_index, workspace, workspace_size, false);
+}
+
+int dsattn_attn_fwd_reordered_noalloc(const dsattn_args* args, const int32_t* q_index,
+                                      const int32_t* kv_index) {
+  if (args == nullptr) return fail(DSATTN_EINVAL, "args must be non-null");
+  void* ws = nullptr;
+  // an empty problem touches no scratch
+  if (args->B != 0 && args->H != 0 && args->N != 0) {
+    const int rc = static_scratch(&ws);
+    if (rc != DSATTN_OK) return rc;
+  }
+  return reordered(args, q_index, kv_index, ws, kStaticScratchBytes, true);
 }
 
 namespace {
