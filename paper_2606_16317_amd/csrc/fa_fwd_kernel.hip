@@ -353,13 +353,19 @@ __device__ __forceinline__ void mask_tail(f32x16 (&st)[2], int key0, int N, int 
       if (32 * b + (v >> 2) * 8 + (v & 3) >= lim) st[b][v] = -__builtin_inff();
 }
 
+// Row maxima use IEEE maximum (v_maximum3_f32): with no NaN in the scores it equals fmaxf,
+// and unlike fmaxf it needs no canonicalising copy of its operands.
+__device__ __forceinline__ float fmax_row(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+
 __device__ __forceinline__ float row_max(const f32x16 (&st)[2]) {
   float mx = st[0][0];
 #pragma unroll
-  for (int v = 1; v < 16; ++v) mx = fmaxf(mx, st[0][v]);
+  for (int v = 1; v < 16; ++v) mx = fmax_row(mx, st[0][v]);
 #pragma unroll
-  for (int v = 0; v < 16; ++v) mx = fmaxf(mx, st[1][v]);
-  return half_max(mx);
+  for (int v = 0; v < 16; ++v) mx = fmax_row(mx, st[1][v]);
+  const uint32_t b = __builtin_bit_cast(uint32_t, mx);
+  const auto sw = __builtin_amdgcn_permlane32_swap(b, b, false, false);
+  return fmax_row(__builtin_bit_cast(float, (uint32_t)sw[0]), __builtin_bit_cast(float, (uint32_t)sw[1]));
 }
 
 struct RowState {
@@ -419,19 +425,20 @@ __device__ __forceinline__ void kept_tile(RowState& rs, f32x16 (&o)[4], const f3
   const float neg_m = contribute ? -rs.m_ref : -__builtin_inff();
   float xs[32];
   bf16x8 pf[4];
-  bf16x8 ka[3], va[3];
-  ka[0] = k_operand(kt, 0, r, g);
-  ka[1] = k_operand(kt, 1, r, g);
+  constexpr int RK = 3;   // operand ring: reads issued two MFMAs ahead
+  bf16x8 ka[RK], va[RK];
+#pragma unroll
+  for (int i = 0; i < RK - 1; ++i) ka[i] = k_operand(kt, i, r, g);
   sched_fence();
   __builtin_amdgcn_s_setprio(1);
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
-    if (i + 2 < 16)
-      ka[(i + 2) % 3] = k_operand(kt, i + 2, r, g);
+    if (i + RK - 1 < 16)
+      ka[(i + RK - 1) % RK] = k_operand(kt, i + RK - 1, r, g);
     else
-      va[i - 14] = v_operand(vt, i - 14, lane);
+      va[i + RK - 1 - 16] = v_operand(vt, i + RK - 1 - 16, lane);
     f32x16& acc = s_next[i & 1];
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[i % 3], qf[i >> 1],
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[i % RK], qf[i >> 1],
                                                   i < 2 ? f32x16{} : acc, 0, 0, 0);
     // elements 0-23 here: two under each of the first eight MFMAs, one under the rest
     if (i < 8) {
@@ -444,8 +451,8 @@ __device__ __forceinline__ void kept_tile(RowState& rs, f32x16 (&o)[4], const f3
   }
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
-    if (i + 2 < 16) va[(i + 2) % 3] = v_operand(vt, i + 2, lane);
-    o[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i % 3], pf[i >> 2], o[i & 3], 0, 0, 0);
+    if (i + RK - 1 < 16) va[(i + RK - 1) % RK] = v_operand(vt, i + RK - 1, lane);
+    o[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i % RK], pf[i >> 2], o[i & 3], 0, 0, 0);
     // elements 24-31 (P block 3, first read by MFMA 12) under the first eight
     if (i < 8) softmax_elem_keep(s_cur, 24 + i, c, neg_m, xs, pf);
     sched_fence();
@@ -501,15 +508,16 @@ __device__ __forceinline__ void kept_tile_q8(RowState& rs, f32x16 (&o)[4],
 // Skipped tile j: only S_{j+1} = K_{j+1} Q^T.
 __device__ __forceinline__ void skipped_tile(f32x16 (&s_next)[2], const uint16_t* kt,
                                              const bf16x8 (&qf)[8], int r, int g) {
-  bf16x8 ka[3];
-  ka[0] = k_operand(kt, 0, r, g);
-  ka[1] = k_operand(kt, 1, r, g);
+  constexpr int RK = 3;   // operand ring: reads issued two MFMAs ahead
+  bf16x8 ka[RK];
+#pragma unroll
+  for (int i = 0; i < RK - 1; ++i) ka[i] = k_operand(kt, i, r, g);
   sched_fence();
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
-    if (i + 2 < 16) ka[(i + 2) % 3] = k_operand(kt, i + 2, r, g);
+    if (i + RK - 1 < 16) ka[(i + RK - 1) % RK] = k_operand(kt, i + RK - 1, r, g);
     f32x16& acc = s_next[i & 1];
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[i % 3], qf[i >> 1],
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[i % RK], qf[i >> 1],
                                                   i < 2 ? f32x16{} : acc, 0, 0, 0);
     sched_fence();
   }
