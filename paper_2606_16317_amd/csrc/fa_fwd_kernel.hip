@@ -82,9 +82,10 @@ constexpr float kRescaleSlack = 8.0f;        // log2 units
 struct Smem {
   alignas(16) uint16_t k[2][kTileElems];     // bf16 K tiles, or MX-FP8 K tiles (first half)
   alignas(16) uint16_t v[2][kTileElems];
-  alignas(4) uint8_t vote[2][kWaves];        // per wave: 1 while its last vote here was skip
+  // Per wave, double-buffered by step.  64- and 128-key decisions: 1 while the wave's last
+  // vote here was skip.  32-key decisions: the wave's vote bits on the next tile.
+  alignas(4) uint8_t vote[2][kWaves];
   alignas(16) uint8_t ks[2][kTK * 4];        // MX-FP8 K: E8M0 exponents, 4 blocks per key
-  alignas(4) uint8_t vote_h1[2][kWaves];     // B_c = 32: second-half votes
   alignas(4) uint8_t vote_mid[kWaves];       // B_c = 32: second-half votes taken mid-step
 };
 
@@ -390,6 +391,13 @@ __device__ __forceinline__ void rescale_if_needed(RowState& rs, f32x16 (&o)[4], 
     rs.m_ref = m_new;
   }
 }
+
+// An empty asm statement that reads x: the value must exist at this point of the
+// instruction stream.  With 32-key decisions the consumers of a softmax sit under branches;
+// this keeps its exponentials under the S_{j+1} MFMAs that hide them instead of letting the
+// compiler sink them into the branches, after the MFMAs.
+__device__ __forceinline__ void pin_here(float x) { asm volatile("" ::"v"(x)); }
+__device__ __forceinline__ void pin_here(const bf16x8& x) { asm volatile("" ::"v"(x)); }
 
 // Softmax numerator of S^T element e (0..31, block e / 16, register e % 16).
 __device__ __forceinline__ void softmax_elem(const f32x16 (&st)[2], int e, float c, float neg_m,
@@ -966,10 +974,13 @@ __device__ __forceinline__ void qk_softmax_halves(const f32x16 (&s_cur)[2], floa
     if (i < 8) {
       softmax_elem(s_cur, 2 * i, c, neg_m0, psum0, pf);
       softmax_elem(s_cur, 2 * i + 1, c, neg_m0, psum0, pf);
+      pin_here(psum0);
     } else {
       softmax_elem(s_cur, 2 * i, c, neg_m1, psum1, pf);
       softmax_elem(s_cur, 2 * i + 1, c, neg_m1, psum1, pf);
+      pin_here(psum1);
     }
+    if ((i & 3) == 3) pin_here(pf[i >> 2]);
     sched_fence();
   }
   __builtin_amdgcn_s_setprio(0);
@@ -999,6 +1010,8 @@ __device__ __forceinline__ void qk_softmax_halves_q8(const f32x16 (&s_cur)[2], f
       else
         softmax_elem(s_cur, 8 * i + e, c, neg_m1, psum1, pf);
     }
+    pin_here(i < 2 ? psum0 : psum1);
+    pin_here(pf[i]);
     sched_fence();
   }
   __builtin_amdgcn_s_setprio(0);
@@ -1029,24 +1042,58 @@ __device__ __forceinline__ void pv_second_half(f32x16 (&o)[4], const bf16x8 (&pf
   __builtin_amdgcn_s_setprio(0);
 }
 
+// Votes of this wave's rows on the two 32-key halves h0, h1 of the next tile, one bit each
+// (a bit is set when some valid row keeps):
+//   1  h0 is kept (Eq. 5 against the state after this tile),
+//   2  h1 is kept against the same state (its decision when h0 is skipped),
+//   4  h1 is kept once h0 is.  BLASST: exact, the running max then being max(m, m_h0).
+//      DynSparse: a sufficient condition.  h0 adds at most 32 terms of at most 2^m_h0, so
+//      the LSE afterwards is at most max(LSE, m_h0 + 5) + 1 (log2 units); 1/16 more covers
+//      the rounding of the kernel's own sum and logarithm.  A decision unit without this
+//      bit decides h1 mid-step against the LSE that includes h0.
+// Contraction is off so that every comparison sees the rounded m_hat, as the mid-step
+// decision does.
+template <int RULE>
+__device__ __forceinline__ uint32_t half_votes(const RowState& rs, const float (&mh)[2],
+                                               const LoopCtx& cx) {
+#pragma clang fp contract(off)
+  float ref, ref1;
+  if constexpr (RULE == kRuleDynSparse) {
+    ref = rs.m_ref + log2_fast(half_sum(rs.l_half));
+    ref1 = fmaxf(ref, mh[0] + 5.0f) + 1.0625f;
+  } else {
+    ref = rs.m_true;
+    ref1 = fmaxf(rs.m_true, mh[0]);
+  }
+  const bool k0 = !(mh[0] - ref < cx.thr);
+  const bool k1 = !(mh[1] - ref < cx.thr);
+  const bool s1 = !(mh[1] - ref1 < cx.thr);
+  return (__ballot(cx.valid & k0) != 0 ? 1u : 0u) | (__ballot(cx.valid & k1) != 0 ? 2u : 0u) |
+         (__ballot(cx.valid & s1) != 0 ? 4u : 0u);
+}
+
 // One 64-key step j with 32-key decisions.  On entry s_cur holds S_j and mh its half row
-// maxima (log2 units); vote[0] / vote[1] are the workgroup's vote words for h0 and for h1
-// against the same LSE (used for h1 when h0 is skipped), own[0] / own[1] this wave's own
-// votes (the decisions of 32-row units).  On exit the same for tile j+1.
+// maxima (log2 units); vote[b] is nonzero when some wave of the workgroup set bit b of
+// half_votes for tile j (the decisions of 128-row units), own[b] this wave's bit (those
+// of 32-row units); lds_bytes mirrors this wave's bytes in the two vote buffers, which
+// are stored only when they change.  On exit the same for tile j+1.
 template <int RULE, int UNIT, bool Q8>
 __device__ __forceinline__ void half_tile_step(int j, const f32x16 (&s_cur)[2],
                                                f32x16 (&s_next)[2], float (&mh)[2],
-                                               uint32_t (&vote)[2], bool (&own)[2],
+                                               uint32_t (&vote)[3], bool (&own)[3],
+                                               uint32_t& lds_bytes,
                                                bool& v_ready, RowState& rs, f32x16 (&o)[4],
                                                const typename QFragOf<Q8>::type& qf,
                                                Smem& sm, const LoopCtx& cx, SkipCount& sk) {
   const int nb = (j + 1) & 1;
   const bool has_next = (j + 1) < cx.n_kt;
   load_k_tile<Q8>(sm, j & 1, cx, (j + 2) * kTK);
-  bool keep0 = true, keep1_pre = true, need_v = true;
+  bool keep0 = true, keep1_pre = true, sure1 = true, need_v = true;
   if constexpr (RULE != kRuleDense) {
     const bool any0 = __builtin_amdgcn_readfirstlane(vote[0]) != 0;
     const bool any1 = __builtin_amdgcn_readfirstlane(vote[1]) != 0;
+    const bool anys = __builtin_amdgcn_readfirstlane(vote[2]) != 0;
+    sure1 = UNIT == kTQ ? anys : __builtin_amdgcn_readfirstlane((int)own[2]) != 0;
     need_v = any0 || any1;
     // (readfirstlane keeps the 32-row units' own votes visibly wave-uniform, so the
     // compiler branches on them instead of predicating both paths)
@@ -1080,20 +1127,27 @@ __device__ __forceinline__ void half_tile_step(int j, const f32x16 (&s_cur)[2],
     keep1 = true;
     if (keep0) {
       rs.l_half += psum0;
+      // h1 after h0: from the sure bit, or decided here against the state that includes h0
+      // (DynSparse without a sure vote; the first tile, which has no votes).  The sure bit
+      // is uniform over the decision unit, so every wave of the workgroup meets the barrier.
+      const bool exact = RULE != kRuleDense && !sure1 && (RULE == kRuleDynSparse || j == 0);
       bool own1 = true;
-      if constexpr (RULE != kRuleDense) {
+      if (exact) {
         own1 = __ballot(cx.valid & row_keeps<RULE>(rs, mh[1], cx.thr)) != 0;
         if (UNIT == kTQ && cx.lane == 0) sm.vote_mid[cx.w] = own1 ? 1 : 0;
       }
       sched_fence();
       pv_first_half(o, pf, va, sm.v[j & 1], cx.lane);   // under the vote exchange
       if constexpr (RULE != kRuleDense) {
-        if constexpr (UNIT == kTQ) {
-          asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-          keep1 = __builtin_amdgcn_readfirstlane(
-                      *reinterpret_cast<const uint32_t*>(sm.vote_mid)) != 0;
-        } else {
-          keep1 = __builtin_amdgcn_readfirstlane((int)own1) != 0;
+        keep1 = sure1;
+        if (exact) {
+          if constexpr (UNIT == kTQ) {
+            asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+            keep1 = __builtin_amdgcn_readfirstlane(
+                        *reinterpret_cast<const uint32_t*>(sm.vote_mid)) != 0;
+          } else {
+            keep1 = __builtin_amdgcn_readfirstlane((int)own1) != 0;
+          }
         }
       }
     } else {
@@ -1128,27 +1182,33 @@ __device__ __forceinline__ void half_tile_step(int j, const f32x16 (&s_cur)[2],
   }
   v_ready = need_v;
 
-  bool next_own0 = true, next_own1 = true;
+  bool next_own0 = true, next_own1 = true, next_s1 = true;
   if (has_next) {
     if (cx.ragged && j + 1 == cx.n_kt - 1) mask_tail(s_next, (j + 1) * kTK, cx.N, cx.g);
     mh[0] = block_max(s_next[0]) * cx.c;
     mh[1] = block_max(s_next[1]) * cx.c;
     if constexpr (RULE != kRuleDense) {
-      next_own0 = __ballot(cx.valid & row_keeps<RULE>(rs, mh[0], cx.thr)) != 0;
-      next_own1 = __ballot(cx.valid & row_keeps<RULE>(rs, mh[1], cx.thr)) != 0;
-      if (cx.lane == 0) {
-        sm.vote[nb][cx.w] = next_own0 ? 1 : 0;
-        sm.vote_h1[nb][cx.w] = next_own1 ? 1 : 0;
+      const uint32_t b = half_votes<RULE>(rs, mh, cx);
+      next_own0 = (b & 1u) != 0;
+      next_own1 = (b & 2u) != 0;
+      next_s1 = (b & 4u) != 0;
+      const uint32_t sh = 8u * (uint32_t)nb;
+      if (((lds_bytes >> sh) & 0xffu) != b) {
+        if (cx.lane == 0) sm.vote[nb][cx.w] = (uint8_t)b;
+        lds_bytes ^= (((lds_bytes >> sh) & 0xffu) ^ b) << sh;
       }
     }
   }
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
   if (has_next) {
     if constexpr (RULE != kRuleDense) {
-      vote[0] = *reinterpret_cast<const uint32_t*>(sm.vote[nb]);
-      vote[1] = *reinterpret_cast<const uint32_t*>(sm.vote_h1[nb]);
+      const uint32_t word = *reinterpret_cast<const uint32_t*>(sm.vote[nb]);
+      vote[0] = word & 0x01010101u;
+      vote[1] = word & 0x02020202u;
+      vote[2] = word & 0x04040404u;
       own[0] = next_own0;
       own[1] = next_own1;
+      own[2] = next_s1;
     }
   }
 }
@@ -1292,14 +1352,17 @@ fa_fwd_kernel(FwdParams p) {
   if constexpr (HALF) {
     static_assert(ORDER == kOrderAscending, "32-key decisions walk keys in ascending order");
     float mh[2] = {block_max(sa[0]) * cx.c, block_max(sa[1]) * cx.c};
-    uint32_t votes[2] = {1u, 1u};            // h0 of the first tile is always kept
-    bool own[2] = {true, true};
+    // h0 of the first tile is always kept and its h1 decided mid-step; the vote buffers
+    // were cleared above.
+    uint32_t votes[3] = {1u, 1u, 0u};
+    bool own[3] = {true, true, false};
+    uint32_t lds_bytes = 0u;
     for (int j = 0; j < cx.n_kt; j += 2) {
-      half_tile_step<RULE, UNIT, Q8>(j, sa, sb, mh, votes, own, v_ready, rs, o, qf, sm, cx,
-                                     sk);
+      half_tile_step<RULE, UNIT, Q8>(j, sa, sb, mh, votes, own, lds_bytes, v_ready, rs, o, qf,
+                                     sm, cx, sk);
       if (j + 1 < cx.n_kt)
-        half_tile_step<RULE, UNIT, Q8>(j + 1, sb, sa, mh, votes, own, v_ready, rs, o, qf, sm,
-                                       cx, sk);
+        half_tile_step<RULE, UNIT, Q8>(j + 1, sb, sa, mh, votes, own, lds_bytes, v_ready, rs, o,
+                                       qf, sm, cx, sk);
     }
   } else if constexpr (PAIR) {
     // Ascending: the last pair is the partial one and may end after one step.  Diagonal:

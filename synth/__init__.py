@@ -14,6 +14,7 @@ from .video_qkv import (
     make_video_qkv,
     workload_inputs,
 )
+from .half_flip import half_flip_inputs
 from .margin_band import margin_band_inputs
 from .vote_patterns import expected_skip, vote_pattern_inputs
 
@@ -27,5 +28,6 @@ __all__ = [
     "workload_inputs",
     "vote_pattern_inputs",
     "margin_band_inputs",
+    "half_flip_inputs",
     "expected_skip",
 ]
