@@ -61,6 +61,12 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="wan720p")
     ap.add_argument("--recall", type=float, default=None, help="recall target (default: workload's)")
+    ap.add_argument("--lam", type=float, default=None,
+                    help="time DynSparse at this fixed lambda instead of a recall target "
+                         "(profiling of the sparse path)")
+    ap.add_argument("--tag", default="",
+                    help="suffix of the traffic record read or written "
+                         "(profiles/hbm_traffic_<workload>[_<tag>].json)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate wall-clock budget of the oracle baseline (0 = skip)")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense timing (profiling)")
@@ -81,6 +87,9 @@ def parse():
                     help="skip the hipBLASLt bf16 GEMM reference rate")
     ap.add_argument("--trace-summary", default=None, metavar="DIR",
                     help="summarise a rocprofv3 --kernel-trace --stats csv output dir and exit")
+    ap.add_argument("--counter-summary", nargs="+", default=None, metavar="DIR",
+                    help="summarise rocprofv3 --pmc csv output dirs (SQ / GRBM counters of "
+                         "the attention kernels) and exit")
     ap.add_argument("--traffic-summary", nargs=2, default=None, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of "
                          "`bench.py --calib-copy` into profiles/hbm_traffic_<workload>.json")
@@ -129,10 +138,15 @@ def kernel_source_digest():
     return hashlib.sha256(open(src, "rb").read()).hexdigest()
 
 
-def measured_traffic(workload):
+def traffic_path(workload, tag=""):
+    return os.path.join(ROOT, "profiles",
+                        f"hbm_traffic_{workload}{'_' + tag if tag else ''}.json")
+
+
+def measured_traffic(workload, tag=""):
     """HBM bytes per launch of the DynSparse kernel from the committed rocprofv3 counter
     summary, or None when there is none or the kernel source changed since."""
-    path = os.path.join(ROOT, "profiles", f"hbm_traffic_{workload}.json")
+    path = traffic_path(workload, tag)
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
@@ -424,9 +438,12 @@ def main():
     if args.trace_summary:
         print(trace_summary(args.trace_summary, args.command))
         return
+    if args.counter_summary:
+        print(counter_summary(args.counter_summary, args.command))
+        return
     if args.traffic_summary:
         rec = traffic_summary(*args.traffic_summary, args.workload, args.command)
-        path = os.path.join(ROOT, "profiles", f"hbm_traffic_{args.workload}.json")
+        path = traffic_path(args.workload, args.tag)
         with open(path, "w") as fh:
             json.dump(rec, fh, indent=1)
         print(json.dumps(rec))
@@ -464,19 +481,26 @@ def main():
 def headline(args, dsa, w, q, k, v, leg):
     import torch
 
-    recall = w.recall if args.recall is None else args.recall
     B, H, N = w.B, w.H, w.N
-    lam = dsa.dsattn_lambda_from_recall(recall, N)
+    fixed = args.lam is not None
+    recall = None if fixed else (w.recall if args.recall is None else args.recall)
+    lam = args.lam if fixed else dsa.dsattn_lambda_from_recall(recall, N)
+    rule, param = ("dynsparse_lambda", lam) if fixed else ("dynsparse_recall", recall)
     L = Layer(dsa, w, q, k, v, args.steps, args.warmup, dense=not args.no_dense)
     n_qt, n_kt = -(-N // TILE_Q), -(-N // TILE_K)
     mask = torch.empty(B * H * n_qt * n_kt, dtype=torch.uint8, device="cuda")
     print(f"[bench] dynsparse recall={recall} lambda={lam:.3f}: {args.warmup} warmup + "
           f"{args.steps} timed steps", file=sys.stderr, flush=True)
 
-    # the timed step: dynsparse_attn_fwd (named entry point) with stats
+    # the timed step: dynsparse_attn_fwd (named entry point) with stats, or its fixed-lambda
+    # variant
     def step():
-        dsa.dynsparse_attn_fwd(L.qd, L.kd, L.vd, L.o, scale=L.scale, recall_target=recall,
-                               stats_out=L.stats)
+        if fixed:
+            dsa.dynsparse_attn_fwd_lambda(L.qd, L.kd, L.vd, L.o, scale=L.scale, lam=lam,
+                                          stats_out=L.stats)
+        else:
+            dsa.dynsparse_attn_fwd(L.qd, L.kd, L.vd, L.o, scale=L.scale, recall_target=recall,
+                                   stats_out=L.stats)
 
     ms = time_calls(step, args.steps, args.warmup)
     st = L.stats.cpu().numpy().reshape(B * H, 4)
@@ -484,9 +508,9 @@ def headline(args, dsa, w, q, k, v, leg):
     achieved = flop_alg / (ms * 1e-3) / 1e12
     # outside the timed region: LSE, mask and output of the same rule for recall, error
     # and the oracle comparison
-    rec = L.measure("dynsparse_recall", recall, mask=mask, time_it=False)
+    rec = L.measure(rule, param, mask=mask, time_it=False)
 
-    traffic = measured_traffic(w.name)
+    traffic = measured_traffic(w.name, args.tag)
     if args.calib_copy:
         src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
@@ -501,7 +525,7 @@ def headline(args, dsa, w, q, k, v, leg):
         m = mask.cpu().numpy().reshape(B * H, n_qt, n_kt)
         o_np = L.o.view(torch.int16).cpu().numpy().view("uint16").reshape(B * H, N, D)
         _, heads = leg.paths[w.name]
-        name, thr = oracle_threshold("dynsparse_recall", recall, N)
+        name, thr = oracle_threshold(rule, param, N)
         res = leg.run(w.name, name, thr, spread_tiles(heads, n_qt, 64), mask=m, o=o_np,
                       budget_s=args.cpu_seconds)
         cpu = cpu_baseline_record(res, N, leg.workers, leg.info, w.name)
@@ -645,6 +669,57 @@ def trace_summary(d, command):
         short = name if len(name) < 90 else name[:87] + "..."
         lines.append(f"{int(r['Calls']):>6} {float(r['AverageNs']) / 1e6:>10.3f} "
                      f"{float(r['TotalDurationNs']) / 1e6:>10.3f} {float(r['Percentage']):>6.2f}  {short}")
+    return "\n".join(lines)
+
+
+# gfx950: 8 accelerator dies (GRBM_GUI_ACTIVE is summed over them), 256 CUs x 4 SIMDs
+XCDS, SIMDS = 8, 1024
+KERNEL_RULES = {"0": "dense", "1": "blasst", "2": "dynsparse"}
+
+
+def counter_summary(dirs, command):
+    """Text summary of rocprofv3 --pmc passes (one dir per pass) over the attention kernels
+    (128-row units, ascending order, bf16, 64-key tiles): the last dispatch's value of each
+    counter, then per-SIMD and per-wave-cycle ratios.  SQ_*_CYCLES / SQ_WAIT_* /
+    SQ_ACTIVE_INST_* count per wave (in the same unit as SQ_WAVE_CYCLES), summed over the
+    chip; SQ_VALU_MFMA_BUSY_CYCLES counts per SIMD."""
+    import csv
+
+    vals = {}
+    for d in dirs:
+        for r in csv.DictReader(open(_find_csv(d, "counter_collection.csv"))):
+            m = re.search(r"fa_fwd_kernel<(\d), 128, 0, false, 64>", r["Kernel_Name"])
+            if not m:
+                continue
+            kern = KERNEL_RULES[m.group(1)]
+            vals.setdefault(kern, {}).setdefault(r["Counter_Name"], []).append(
+                float(r["Counter_Value"]))
+    lines = ["# rocprofv3 --pmc summary: SQ / GRBM counters of the attention kernels",
+             f"# command: {command}",
+             "# values: last dispatch of each kernel (counts summed over the chip)"]
+    for kern, cs in vals.items():
+        last = {c: v[-1] for c, v in cs.items()}
+        lines.append(f"kernel fa_fwd_kernel<{kern}>  dispatches per pass: "
+                     f"{min(len(v) for v in cs.values())}")
+        for c in sorted(last):
+            lines.append(f"  {c:<30} {last[c]:.5g}")
+        cyc = last.get("GRBM_GUI_ACTIVE", 0.0) / XCDS
+        if cyc and "SQ_VALU_MFMA_BUSY_CYCLES" in last:
+            lines.append(f"  = MFMA busy per SIMD per cycle        "
+                         f"{last['SQ_VALU_MFMA_BUSY_CYCLES'] / SIMDS / cyc:.3f}")
+        wave = last.get("SQ_WAVE_CYCLES")
+        if wave:
+            for c in ("SQ_ACTIVE_INST_ANY", "SQ_ACTIVE_INST_VALU", "SQ_ACTIVE_INST_LDS",
+                      "SQ_ACTIVE_INST_SCA", "SQ_ACTIVE_INST_MISC", "SQ_ACTIVE_INST_VMEM",
+                      "SQ_WAIT_INST_ANY", "SQ_WAIT_INST_LDS", "SQ_WAIT_ANY", "SQ_BUSY_CYCLES"):
+                if c in last:
+                    lines.append(f"  = {c:<30} per wave cycle {last[c] / wave:.3f}")
+        mfma = last.get("SQ_INSTS_MFMA")
+        if mfma:
+            for c in ("SQ_INSTS_VALU", "SQ_INSTS_VALU_TRANS_F32", "SQ_INSTS_LDS",
+                      "SQ_INSTS_SALU", "SQ_INSTS_BRANCH"):
+                if c in last:
+                    lines.append(f"  = {c:<30} per MFMA {last[c] / mfma:.3f}")
     return "\n".join(lines)
 
 
