@@ -669,6 +669,39 @@ def trace_summary(d, command):
         short = name if len(name) < 90 else name[:87] + "..."
         lines.append(f"{int(r['Calls']):>6} {float(r['AverageNs']) / 1e6:>10.3f} "
                      f"{float(r['TotalDurationNs']) / 1e6:>10.3f} {float(r['Percentage']):>6.2f}  {short}")
+    # The attention kernels per run of consecutive dispatches with one launch shape (in
+    # issue order: each timed configuration is such a run), from the dispatch list
+    try:
+        trace = _find_csv(d, "kernel_trace.csv")
+    except FileNotFoundError:
+        return "\n".join(lines)
+    disp = []
+    for r in csv.DictReader(open(trace)):
+        m = re.search(r"(fa_fwd_(?:mask_)?kernel<[^>]*>)", r["Kernel_Name"])
+        if not m:
+            continue
+        disp.append((int(r["Start_Timestamp"]), m.group(1),
+                     f"{int(r['Grid_Size_X']) // max(1, int(r['Workgroup_Size_X']))}x"
+                     f"{r['Grid_Size_Y']}", r["Scratch_Size"], r["LDS_Block_Size"],
+                     int(r["End_Timestamp"]) - int(r["Start_Timestamp"])))
+    disp.sort()
+    runs = []
+    for _, name, grid, scr, lds, ns in disp:
+        # a new run where the shape changes, or where the time moves more than 4 % from
+        # the run's mean (another threshold on the same kernel)
+        if runs and runs[-1][0] == (name, grid, scr, lds) and \
+                abs(ns - sum(runs[-1][1]) / len(runs[-1][1])) <= 0.04 * sum(runs[-1][1]) / len(runs[-1][1]):
+            runs[-1][1].append(ns)
+        else:
+            runs.append(((name, grid, scr, lds), [ns]))
+    lines += ["", "# attention kernels, runs of consecutive dispatches in issue order, split "
+                  "where the shape changes or the time moves by more than 4 % (grid in "
+                  "workgroups; scratch and LDS bytes per workgroup)",
+              f"{'run':>4} {'calls':>6} {'avg_ms':>10} {'min_ms':>10}  {'grid':>10} "
+              f"{'scratch':>7} {'lds':>6}  kernel"]
+    for n, ((name, grid, scr, lds), ns) in enumerate(runs):
+        lines.append(f"{n:>4} {len(ns):>6} {sum(ns) / len(ns) / 1e6:>10.3f} "
+                     f"{min(ns) / 1e6:>10.3f}  {grid:>10} {scr:>7} {lds:>6}  {name}")
     return "\n".join(lines)
 
 
