@@ -18,6 +18,14 @@ every point of the threshold sweep, and the stress layer, each with throughput,
 roofline fraction, speedup over dense, sparsity, relative L2 against dense, achieved
 recall and the oracle mismatch count on sampled query tiles.
 
+``--lam L`` times DynSparse at a fixed threshold instead of the recall target (the sparse
+path, for profiling); ``--tag`` names the traffic record that line reads.
+
+``--trace-summary``, ``--counter-summary`` and ``--traffic-summary`` turn rocprofv3 output
+(kernel trace with stats; SQ/GRBM counter passes; FETCH_SIZE and WRITE_SIZE passes of a
+``--calib-copy`` run) into the summaries kept under ``profiles/``; each summary records the
+command that produced its input.
+
 ``--sweep`` instead prints one JSON line per rule/threshold on the given workload;
 ``--reorder-sweep`` prints, per rule/threshold, the row-major run next to the same run over
 the spatio-temporally blocked token order (``dsattn_attn_fwd_reordered``, gathers and the
