@@ -584,6 +584,10 @@ struct LoopCtx {
   uint8_t* mask_row;            // this decision unit's row of the skip mask, or null
   float c;
   float thr;
+  // The rule's threshold on this lane's query row, +inf past the last row: a vote taken
+  // against it is "skip" for rows past N (their margin is finite once a tile is kept, and
+  // every vote follows the first kept tile), so the votes need no row mask.
+  float thr_row;
   int N, n_kt, w, lane, r, g;
   int rows_valid;               // valid query rows of this decision unit
   bool valid, ragged;
@@ -641,9 +645,11 @@ __device__ __forceinline__ void store_rows(const FwdParams& p, const f32x16 (&o)
   }
 }
 
+// Skipped key tiles (or 32-key halves) of one decision unit, and the keys they hold; the
+// skipped elements are rows_valid times the keys, formed once after the loop.
 struct SkipCount {
   uint32_t tiles = 0;
-  uint64_t elems = 0;
+  uint32_t keys = 0;
 };
 
 // Stage the K tile starting at key key0 into K buffer buf (bf16, or MX-FP8 codes and
@@ -726,7 +732,7 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
       rs.lse = rs.m_ref + log2_fast(half_sum(rs.l_half));
   } else {
     sk.tiles += 1;
-    sk.elems += (uint64_t)cx.rows_valid * (uint64_t)min(kTK, cx.N - tj * kTK);
+    sk.keys += (uint32_t)min(kTK, cx.N - tj * kTK);
     if constexpr (Q8)
       skipped_tile_q8(s_next, reinterpret_cast<const uint8_t*>(sm.k[nb]), sm.ks[nb], qf, cx.r,
                       cx.g);
@@ -741,8 +747,8 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
     if (cx.ragged && tn == cx.n_kt - 1) mask_tail(s_next, tn * kTK, cx.N, cx.g);
     mhat_next = row_max(s_next) * cx.c;
     if constexpr (RULE != kRuleDense) {
-      wave_keeps = __ballot(cx.valid & (Q8 ? row_keeps_cached<RULE>(rs, mhat_next, cx.thr)
-                                              : row_keeps<RULE>(rs, mhat_next, cx.thr))) != 0;
+      wave_keeps = __ballot(Q8 ? row_keeps_cached<RULE>(rs, mhat_next, cx.thr_row)
+                               : row_keeps<RULE>(rs, mhat_next, cx.thr_row)) != 0;
       const uint32_t mark = wave_keeps ? 0u : 1u;
       if (mark != ((marks >> nb) & 1u)) {
         if (cx.lane == 0) sm.vote[nb][cx.w] = (uint8_t)mark;
@@ -850,7 +856,7 @@ __device__ __forceinline__ void pair_first_step(int j, const f32x16 (&s_cur)[2],
   if ((tj + 2) * kTK > cx.N) mask_tail(s_next, (tj + 1) * kTK, cx.N, cx.g);
   const float mhat_pair = fmaxf(mhat, row_max(s_next) * cx.c);
   if constexpr (RULE != kRuleDense) {
-    const bool wave_keeps = __ballot(cx.valid & row_keeps<RULE>(rs, mhat_pair, cx.thr)) != 0;
+    const bool wave_keeps = __ballot(row_keeps<RULE>(rs, mhat_pair, cx.thr_row)) != 0;
     if (cx.lane == 0) sm.vote[0][cx.w] = wave_keeps ? 1 : 0;
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
     keep_any = __builtin_amdgcn_readfirstlane(*reinterpret_cast<const uint32_t*>(sm.vote[0])) != 0;
@@ -868,7 +874,7 @@ __device__ __forceinline__ void pair_first_step(int j, const f32x16 (&s_cur)[2],
     softmax_pv_tile(rs, o, s_cur, cx.c, sm.v[j & 1], cx.lane);
   } else {
     sk.tiles += 1;
-    sk.elems += (uint64_t)cx.rows_valid * (uint64_t)min(2 * kTK, cx.N - tj * kTK);
+    sk.keys += (uint32_t)min(2 * kTK, cx.N - tj * kTK);
   }
   v_ready = keep_any;
   mhat = mhat_pair;
@@ -1065,11 +1071,11 @@ __device__ __forceinline__ uint32_t half_votes(const RowState& rs, const float (
     ref = rs.m_true;
     ref1 = fmaxf(rs.m_true, mh[0]);
   }
-  const bool k0 = !(mh[0] - ref < cx.thr);
-  const bool k1 = !(mh[1] - ref < cx.thr);
-  const bool s1 = !(mh[1] - ref1 < cx.thr);
-  return (__ballot(cx.valid & k0) != 0 ? 1u : 0u) | (__ballot(cx.valid & k1) != 0 ? 2u : 0u) |
-         (__ballot(cx.valid & s1) != 0 ? 4u : 0u);
+  const bool k0 = !(mh[0] - ref < cx.thr_row);
+  const bool k1 = !(mh[1] - ref < cx.thr_row);
+  const bool s1 = !(mh[1] - ref1 < cx.thr_row);
+  return (__ballot(k0) != 0 ? 1u : 0u) | (__ballot(k1) != 0 ? 2u : 0u) |
+         (__ballot(s1) != 0 ? 4u : 0u);
 }
 
 // One 64-key step j with 32-key decisions.  On entry s_cur holds S_j and mh its half row
@@ -1133,7 +1139,7 @@ __device__ __forceinline__ void half_tile_step(int j, const f32x16 (&s_cur)[2],
       const bool exact = RULE != kRuleDense && !sure1 && (RULE == kRuleDynSparse || j == 0);
       bool own1 = true;
       if (exact) {
-        own1 = __ballot(cx.valid & row_keeps<RULE>(rs, mh[1], cx.thr)) != 0;
+        own1 = __ballot(row_keeps<RULE>(rs, mh[1], cx.thr_row)) != 0;
         if (UNIT == kTQ && cx.lane == 0) sm.vote_mid[cx.w] = own1 ? 1 : 0;
       }
       sched_fence();
@@ -1174,11 +1180,11 @@ __device__ __forceinline__ void half_tile_step(int j, const f32x16 (&s_cur)[2],
   }
   if (!keep0) {
     sk.tiles += 1;
-    sk.elems += (uint64_t)cx.rows_valid * (uint64_t)min(32, cx.N - j * kTK);
+    sk.keys += (uint32_t)min(32, cx.N - j * kTK);
   }
   if (h1_exists && !keep1) {
     sk.tiles += 1;
-    sk.elems += (uint64_t)cx.rows_valid * (uint64_t)min(32, cx.N - j * kTK - 32);
+    sk.keys += (uint32_t)min(32, cx.N - j * kTK - 32);
   }
   v_ready = need_v;
 
@@ -1272,6 +1278,7 @@ fa_fwd_kernel(FwdParams p) {
   const int q0 = qt * kTQ;
   const int qrow = q0 + cx.w * 32 + cx.r;
   cx.valid = qrow < N;
+  cx.thr_row = cx.valid ? p.thr : __builtin_inff();
   cx.ragged = (N % kTK) != 0;
   // This wave's decision unit: the workgroup's tile, or the wave's own 32 rows.
   const int unit = UNIT == kTQ ? qt : qt * (kTQ / UNIT) + cx.w;
@@ -1394,7 +1401,7 @@ fa_fwd_kernel(FwdParams p) {
     atomicAdd(st + 0, (unsigned long long)(BC == kTK ? cx.n_kt : p.n_kd));
     atomicAdd(st + 1, (unsigned long long)sk.tiles);
     atomicAdd(st + 2, (unsigned long long)cx.rows_valid * (unsigned long long)N);
-    atomicAdd(st + 3, (unsigned long long)sk.elems);
+    atomicAdd(st + 3, (unsigned long long)cx.rows_valid * (unsigned long long)sk.keys);
   }
 }
 
@@ -1480,6 +1487,7 @@ fa_fwd_mask_kernel(FwdParams p) {
   const int q0 = qt * kTQ;
   const int qrow = q0 + cx.w * 32 + cx.r;
   cx.valid = qrow < N;
+  cx.thr_row = cx.valid ? p.thr : __builtin_inff();
   cx.ragged = (N % kTK) != 0;
   const int unit = UNIT == kTQ ? qt : qt * (kTQ / UNIT) + cx.w;
   cx.rows_valid = max(0, min(UNIT, N - unit * UNIT));
