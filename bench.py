@@ -14,7 +14,8 @@ the sampled-tile decision mismatch count).  One JSON line is printed.
 
 ``--all-configs`` prints one JSON line per workload and rule instead: the tiny, 480p and
 720p layers at their recall target (720p also at the paper's lambda = -6 and at -8),
-every point of the threshold sweep, and the stress layer, each with throughput,
+every point of the threshold sweep plus lambda = -6 on its draw, and the stress layer
+(recall target and lambda = -6), each with throughput,
 roofline fraction, speedup over dense, sparsity, relative L2 against dense, achieved
 recall and the oracle mismatch count on sampled query tiles.
 
@@ -592,6 +593,7 @@ ALL_CONFIGS = [("tiny", "dynsparse_recall", 0.95),
                ("wan720p_sweep", "blasst", 1e-2),
                ("wan720p_sweep", "blasst", 1e-3),
                ("wan720p_sweep", "blasst", 1e-4),
+               ("wan720p_sweep", "dynsparse_lambda", -6.0),
                ("wan720p_sweep", "dense", 0.0),
                ("stress", "dynsparse_recall", 0.95),
                ("stress", "dynsparse_lambda", -6.0)]
