@@ -369,6 +369,21 @@ __device__ __forceinline__ float row_max(const f32x16 (&st)[2]) {
   return fmax_row(__builtin_bit_cast(float, (uint32_t)sw[0]), __builtin_bit_cast(float, (uint32_t)sw[1]));
 }
 
+// Four elements of a running lane-local row max over a score tile, elements
+// 1 + 4k .. 4 + 4k (k = 0..7; element 0 starts the chain), for the MFMA slots that carry
+// no other VALU work.
+__device__ __forceinline__ void row_max_part(const f32x16 (&st)[2], int k, float& mx) {
+#pragma unroll
+  for (int e = 1 + 4 * k; e <= 4 + 4 * k && e < 32; ++e) mx = fmax_row(mx, st[e >> 4][e & 15]);
+}
+
+// Combine a lane-local row max with the other lane half of the row.
+__device__ __forceinline__ float row_max_join(float mx) {
+  const uint32_t b = __builtin_bit_cast(uint32_t, mx);
+  const auto sw = __builtin_amdgcn_permlane32_swap(b, b, false, false);
+  return fmax_row(__builtin_bit_cast(float, (uint32_t)sw[0]), __builtin_bit_cast(float, (uint32_t)sw[1]));
+}
+
 struct RowState {
   float m_ref;   // reference max (log2 units) of P = exp2(S*c - m_ref)
   float m_true;  // running max of the kept tiles (BLASST metric)
@@ -425,7 +440,7 @@ __device__ __forceinline__ void kept_tile(RowState& rs, f32x16 (&o)[4], const f3
                                           float m_hat, float c, f32x16 (&s_next)[2],
                                           const uint16_t* kt, const uint16_t* vt,
                                           const bf16x8 (&qf)[8], int r, int g, int lane,
-                                          bool contribute = true) {
+                                          float& rmax_next, bool contribute = true) {
   // contribute == false (uniform): the tile runs the same instructions but adds nothing --
   // exp2(S c - inf) = 0 for every element (S is finite or -inf), and the running max and
   // sum stay as they are.
@@ -461,11 +476,18 @@ __device__ __forceinline__ void kept_tile(RowState& rs, f32x16 (&o)[4], const f3
   for (int i = 0; i < 16; ++i) {
     if (i + RK - 1 < 16) va[(i + RK - 1) % RK] = v_operand(vt, i + RK - 1, lane);
     o[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i % RK], pf[i >> 2], o[i & 3], 0, 0, 0);
-    // elements 24-31 (P block 3, first read by MFMA 12) under the first eight
-    if (i < 8) softmax_elem_keep(s_cur, 24 + i, c, neg_m, xs, pf);
+    // elements 24-31 (P block 3, first read by MFMA 12) under the first eight; the row
+    // max of S_{j+1} (complete by now) under the other eight
+    if (i < 8) {
+      softmax_elem_keep(s_cur, 24 + i, c, neg_m, xs, pf);
+    } else {
+      if (i == 8) rmax_next = s_next[0][0];
+      row_max_part(s_next, i - 8, rmax_next);
+    }
     sched_fence();
   }
   __builtin_amdgcn_s_setprio(0);
+  rmax_next = row_max_join(rmax_next);
   // The row sum goes after the P V MFMAs, where the VALU is otherwise idle, rather than
   // into the softmax phase, which is VALU-bound.
   float psum = 0.f;
@@ -718,14 +740,16 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
   if (keep_any) load_tile_lds(sm.v[nb], cx.vrs, cx.voff, tn * kTK, cx.w);
 
   // S_{j+1} is computed on both paths (on the last tile it reads a stale buffer and is
-  // dropped).
+  // dropped).  A kept tile also takes its row max (of S_{j+1} as computed, before any
+  // tail mask).
+  float rmax_kept = 0.f;
   if (keep_own) {
     if constexpr (Q8)
       kept_tile_q8(rs, o, s_cur, mhat, cx.c, s_next, reinterpret_cast<const uint8_t*>(sm.k[nb]),
                    sm.ks[nb], sm.v[j & 1], qf, cx.r, cx.g, cx.lane);
     else
       kept_tile(rs, o, s_cur, mhat, cx.c, s_next, sm.k[nb], sm.v[j & 1], qf, cx.r, cx.g,
-                cx.lane);
+                cx.lane, rmax_kept);
     // The MX-FP8 path caches the LSE for its votes (its kept tiles are shorter, and taking
     // the log out of the vote chain pays there); the bf16 path keeps it in the chain.
     if constexpr (Q8 && RULE == kRuleDynSparse)
@@ -744,8 +768,16 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
   float mhat_next = 0.f;
   bool wave_keeps = true;
   if (has_next) {
-    if (cx.ragged && tn == cx.n_kt - 1) mask_tail(s_next, tn * kTK, cx.N, cx.g);
-    mhat_next = row_max(s_next) * cx.c;
+    float rmax;
+    if (cx.ragged && tn == cx.n_kt - 1) {
+      mask_tail(s_next, tn * kTK, cx.N, cx.g);
+      rmax = row_max(s_next);
+    } else if (!Q8 && keep_own) {
+      rmax = rmax_kept;
+    } else {
+      rmax = row_max(s_next);
+    }
+    mhat_next = rmax * cx.c;
     if constexpr (RULE != kRuleDense) {
       wave_keeps = __ballot(Q8 ? row_keeps_cached<RULE>(rs, mhat_next, cx.thr_row)
                                : row_keeps<RULE>(rs, mhat_next, cx.thr_row)) != 0;
@@ -894,13 +926,14 @@ __device__ __forceinline__ void pair_second_step(int j, const f32x16 (&s_cur)[2]
   const int tn = pair_tile<ORDER>(j + 1, cx);        // the next pair's first tile
   load_k_tile<Q8>(sm, j & 1, cx, pair_tile<ORDER>(j + 2, cx) * kTK);
   if (keep_any) load_tile_lds(sm.v[nb], cx.vrs, cx.voff, tn * kTK, cx.w);
+  float rmax_unused;                                // (the row max is taken below)
   if (keep_own) {
     if constexpr (Q8)
       kept_tile_q8(rs, o, s_cur, mhat, cx.c, s_next, reinterpret_cast<const uint8_t*>(sm.k[nb]),
                    sm.ks[nb], sm.v[j & 1], qf, cx.r, cx.g, cx.lane);
     else
       kept_tile(rs, o, s_cur, mhat, cx.c, s_next, sm.k[nb], sm.v[j & 1], qf, cx.r, cx.g,
-                cx.lane);
+                cx.lane, rmax_unused);
   } else {
     if constexpr (Q8)
       skipped_tile_q8(s_next, reinterpret_cast<const uint8_t*>(sm.k[nb]), sm.ks[nb], qf, cx.r,
@@ -1441,12 +1474,16 @@ __device__ __forceinline__ void mask_tile_step(int j, int n_keep, const f32x16 (
   // Some unit of the workgroup keeps every visited tile and the step's barrier waits for
   // it, so a wave whose own unit skips the tile runs the kept path without contributing
   // rather than a second code path.
+  float rmax_kept;
   kept_tile(rs, o, s_cur, mhat, cx.c, s_next, sm.t.k[nb], sm.t.v[j & 1], qf, cx.r, cx.g,
-            cx.lane, keep_own);
+            cx.lane, rmax_kept, keep_own);
   float mhat_next = 0.f;
   if (has_next) {
-    if (cx.ragged && tn == cx.n_kt - 1) mask_tail(s_next, tn * kTK, cx.N, cx.g);
-    mhat_next = row_max(s_next) * cx.c;
+    if (cx.ragged && tn == cx.n_kt - 1) {
+      mask_tail(s_next, tn * kTK, cx.N, cx.g);
+      rmax_kept = row_max(s_next);
+    }
+    mhat_next = rmax_kept * cx.c;
   }
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
   mhat = mhat_next;
