@@ -553,6 +553,14 @@ __device__ __forceinline__ void skipped_tile(f32x16 (&s_next)[2], const uint16_t
   }
 }
 
+// Skipped tile j with the row max of S_{j+1} (before any tail mask), taken after its
+// MFMAs.
+__device__ __forceinline__ float skipped_tile_rmax(f32x16 (&s_next)[2], const uint16_t* kt,
+                                                   const bf16x8 (&qf)[8], int r, int g) {
+  skipped_tile(s_next, kt, qf, r, g);
+  return row_max(s_next);
+}
+
 // Skipped tile j on the MX-FP8 path: only S_{j+1}.
 __device__ __forceinline__ void skipped_tile_q8(f32x16 (&s_next)[2], const uint8_t* kt,
                                                 const uint8_t* ks, const QFrag8& qf, int r,
@@ -740,16 +748,16 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
   if (keep_any) load_tile_lds(sm.v[nb], cx.vrs, cx.voff, tn * kTK, cx.w);
 
   // S_{j+1} is computed on both paths (on the last tile it reads a stale buffer and is
-  // dropped).  A kept tile also takes its row max (of S_{j+1} as computed, before any
-  // tail mask).
-  float rmax_kept = 0.f;
+  // dropped), with its row max before any tail mask: under the P V MFMAs of a kept tile,
+  // after the MFMAs of a skipped one.
+  float rmax = 0.f;
   if (keep_own) {
     if constexpr (Q8)
       kept_tile_q8(rs, o, s_cur, mhat, cx.c, s_next, reinterpret_cast<const uint8_t*>(sm.k[nb]),
                    sm.ks[nb], sm.v[j & 1], qf, cx.r, cx.g, cx.lane);
     else
       kept_tile(rs, o, s_cur, mhat, cx.c, s_next, sm.k[nb], sm.v[j & 1], qf, cx.r, cx.g,
-                cx.lane, rmax_kept);
+                cx.lane, rmax);
     // The MX-FP8 path caches the LSE for its votes (its kept tiles are shorter, and taking
     // the log out of the vote chain pays there); the bf16 path keeps it in the chain.
     if constexpr (Q8 && RULE == kRuleDynSparse)
@@ -761,20 +769,15 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
       skipped_tile_q8(s_next, reinterpret_cast<const uint8_t*>(sm.k[nb]), sm.ks[nb], qf, cx.r,
                       cx.g);
     else
-      skipped_tile(s_next, sm.k[nb], qf, cx.r, cx.g);
+      rmax = skipped_tile_rmax(s_next, sm.k[nb], qf, cx.r, cx.g);
   }
   v_ready = keep_any;
 
   float mhat_next = 0.f;
   bool wave_keeps = true;
   if (has_next) {
-    float rmax;
-    if (cx.ragged && tn == cx.n_kt - 1) {
-      mask_tail(s_next, tn * kTK, cx.N, cx.g);
-      rmax = row_max(s_next);
-    } else if (!Q8 && keep_own) {
-      rmax = rmax_kept;
-    } else {
+    if (Q8 || (cx.ragged && tn == cx.n_kt - 1)) {
+      if (cx.ragged && tn == cx.n_kt - 1) mask_tail(s_next, tn * kTK, cx.N, cx.g);
       rmax = row_max(s_next);
     }
     mhat_next = rmax * cx.c;
