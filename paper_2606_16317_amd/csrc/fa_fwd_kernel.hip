@@ -503,7 +503,8 @@ __device__ __forceinline__ void kept_tile_q8(RowState& rs, f32x16 (&o)[4],
                                              const f32x16 (&s_cur)[2], float m_hat, float c,
                                              f32x16 (&s_next)[2], const uint8_t* kt,
                                              const uint8_t* ks, const uint16_t* vt,
-                                             const QFrag8& qf, int r, int g, int lane) {
+                                             const QFrag8& qf, int r, int g, int lane,
+                                             float& rmax_next) {
   rescale_if_needed(rs, o, m_hat);
   const float neg_m = -rs.m_ref;
   float xs[32];
@@ -525,10 +526,16 @@ __device__ __forceinline__ void kept_tile_q8(RowState& rs, f32x16 (&o)[4],
   for (int i = 0; i < 16; ++i) {
     if (i + 2 < 16) va[(i + 2) % 3] = v_operand(vt, i + 2, lane);
     o[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i % 3], pf[i >> 2], o[i & 3], 0, 0, 0);
-    if (i < 8) softmax_elem_keep(s_cur, 24 + i, c, neg_m, xs, pf);   // P block 3, as in kept_tile
+    if (i < 8) {
+      softmax_elem_keep(s_cur, 24 + i, c, neg_m, xs, pf);   // P block 3, as in kept_tile
+    } else {
+      if (i == 8) rmax_next = s_next[0][0];                  // the row max, as in kept_tile
+      row_max_part(s_next, i - 8, rmax_next);
+    }
     sched_fence();
   }
   __builtin_amdgcn_s_setprio(0);
+  rmax_next = row_max_join(rmax_next);
   float psum = 0.f;                          // after the P V MFMAs, as in kept_tile
 #pragma unroll
   for (int e = 0; e < 32; ++e) psum += xs[e];
@@ -573,6 +580,14 @@ __device__ __forceinline__ void skipped_tile_q8(f32x16 (&s_next)[2], const uint8
     qk_q8_step(i, s_next, kf, kt, qf, r, g);
     sched_fence();
   }
+}
+
+// The same with the row max of S_{j+1}, as skipped_tile_rmax.
+__device__ __forceinline__ float skipped_tile_q8_rmax(f32x16 (&s_next)[2], const uint8_t* kt,
+                                                      const uint8_t* ks, const QFrag8& qf,
+                                                      int r, int g) {
+  skipped_tile_q8(s_next, kt, ks, qf, r, g);
+  return row_max(s_next);
 }
 
 // Q operand registers of the bf16 path (eight d-steps) and of the MX-FP8 path.
@@ -754,7 +769,7 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
   if (keep_own) {
     if constexpr (Q8)
       kept_tile_q8(rs, o, s_cur, mhat, cx.c, s_next, reinterpret_cast<const uint8_t*>(sm.k[nb]),
-                   sm.ks[nb], sm.v[j & 1], qf, cx.r, cx.g, cx.lane);
+                   sm.ks[nb], sm.v[j & 1], qf, cx.r, cx.g, cx.lane, rmax);
     else
       kept_tile(rs, o, s_cur, mhat, cx.c, s_next, sm.k[nb], sm.v[j & 1], qf, cx.r, cx.g,
                 cx.lane, rmax);
@@ -766,8 +781,8 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
     sk.tiles += 1;
     sk.keys += (uint32_t)min(kTK, cx.N - tj * kTK);
     if constexpr (Q8)
-      skipped_tile_q8(s_next, reinterpret_cast<const uint8_t*>(sm.k[nb]), sm.ks[nb], qf, cx.r,
-                      cx.g);
+      rmax = skipped_tile_q8_rmax(s_next, reinterpret_cast<const uint8_t*>(sm.k[nb]), sm.ks[nb],
+                                  qf, cx.r, cx.g);
     else
       rmax = skipped_tile_rmax(s_next, sm.k[nb], qf, cx.r, cx.g);
   }
@@ -776,8 +791,8 @@ __device__ __forceinline__ void key_tile_step(int j, const f32x16 (&s_cur)[2], f
   float mhat_next = 0.f;
   bool wave_keeps = true;
   if (has_next) {
-    if (Q8 || (cx.ragged && tn == cx.n_kt - 1)) {
-      if (cx.ragged && tn == cx.n_kt - 1) mask_tail(s_next, tn * kTK, cx.N, cx.g);
+    if (cx.ragged && tn == cx.n_kt - 1) {
+      mask_tail(s_next, tn * kTK, cx.N, cx.g);
       rmax = row_max(s_next);
     }
     mhat_next = rmax * cx.c;
@@ -933,7 +948,7 @@ __device__ __forceinline__ void pair_second_step(int j, const f32x16 (&s_cur)[2]
   if (keep_own) {
     if constexpr (Q8)
       kept_tile_q8(rs, o, s_cur, mhat, cx.c, s_next, reinterpret_cast<const uint8_t*>(sm.k[nb]),
-                   sm.ks[nb], sm.v[j & 1], qf, cx.r, cx.g, cx.lane);
+                   sm.ks[nb], sm.v[j & 1], qf, cx.r, cx.g, cx.lane, rmax_unused);
     else
       kept_tile(rs, o, s_cur, mhat, cx.c, s_next, sm.k[nb], sm.v[j & 1], qf, cx.r, cx.g,
                 cx.lane, rmax_unused);
