@@ -944,25 +944,28 @@ __device__ __forceinline__ void pair_second_step(int j, const f32x16 (&s_cur)[2]
   const int tn = pair_tile<ORDER>(j + 1, cx);        // the next pair's first tile
   load_k_tile<Q8>(sm, j & 1, cx, pair_tile<ORDER>(j + 2, cx) * kTK);
   if (keep_any) load_tile_lds(sm.v[nb], cx.vrs, cx.voff, tn * kTK, cx.w);
-  float rmax_unused;                                // (the row max is taken below)
+  float rmax;                                        // row max of S_{j+1}, as in key_tile_step
   if (keep_own) {
     if constexpr (Q8)
       kept_tile_q8(rs, o, s_cur, mhat, cx.c, s_next, reinterpret_cast<const uint8_t*>(sm.k[nb]),
-                   sm.ks[nb], sm.v[j & 1], qf, cx.r, cx.g, cx.lane, rmax_unused);
+                   sm.ks[nb], sm.v[j & 1], qf, cx.r, cx.g, cx.lane, rmax);
     else
       kept_tile(rs, o, s_cur, mhat, cx.c, s_next, sm.k[nb], sm.v[j & 1], qf, cx.r, cx.g,
-                cx.lane, rmax_unused);
+                cx.lane, rmax);
   } else {
     if constexpr (Q8)
-      skipped_tile_q8(s_next, reinterpret_cast<const uint8_t*>(sm.k[nb]), sm.ks[nb], qf, cx.r,
-                      cx.g);
+      rmax = skipped_tile_q8_rmax(s_next, reinterpret_cast<const uint8_t*>(sm.k[nb]), sm.ks[nb],
+                                  qf, cx.r, cx.g);
     else
-      skipped_tile(s_next, sm.k[nb], qf, cx.r, cx.g);
+      rmax = skipped_tile_rmax(s_next, sm.k[nb], qf, cx.r, cx.g);
   }
   v_ready = keep_any;
   if (tn < cx.n_kt) {
-    if ((tn + 1) * kTK > cx.N) mask_tail(s_next, tn * kTK, cx.N, cx.g);
-    mhat = row_max(s_next) * cx.c;
+    if ((tn + 1) * kTK > cx.N) {
+      mask_tail(s_next, tn * kTK, cx.N, cx.g);
+      rmax = row_max(s_next);
+    }
+    mhat = rmax * cx.c;
   }
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
