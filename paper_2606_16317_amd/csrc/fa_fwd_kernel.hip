@@ -105,11 +105,6 @@ __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0
 
 // Combine a per-lane value with the one held by lane ^ 32 (the other half of the same
 // query row) using v_permlane32_swap: no LDS round trip.
-__device__ __forceinline__ float half_max(float x) {
-  const uint32_t b = __builtin_bit_cast(uint32_t, x);
-  const auto sw = __builtin_amdgcn_permlane32_swap(b, b, false, false);
-  return fmaxf(__builtin_bit_cast(float, (uint32_t)sw[0]), __builtin_bit_cast(float, (uint32_t)sw[1]));
-}
 __device__ __forceinline__ float half_sum(float x) {
   const uint32_t b = __builtin_bit_cast(uint32_t, x);
   const auto sw = __builtin_amdgcn_permlane32_swap(b, b, false, false);
@@ -1003,8 +998,8 @@ __device__ __forceinline__ void raise_reference(RowState& rs, f32x16 (&o)[4], fl
 __device__ __forceinline__ float block_max(const f32x16& st) {
   float mx = st[0];
 #pragma unroll
-  for (int v = 1; v < 16; ++v) mx = fmaxf(mx, st[v]);
-  return half_max(mx);
+  for (int v = 1; v < 16; ++v) mx = fmax_row(mx, st[v]);
+  return row_max_join(mx);
 }
 
 // S_{j+1} = K_{j+1} Q^T with the softmax of both halves of S_j under its 16 MFMAs (block
