@@ -349,8 +349,9 @@ __device__ __forceinline__ void mask_tail(f32x16 (&st)[2], int key0, int N, int 
       if (32 * b + (v >> 2) * 8 + (v & 3) >= lim) st[b][v] = -__builtin_inff();
 }
 
-// Row maxima use IEEE maximum (v_maximum3_f32): with no NaN in the scores it equals fmaxf,
-// and unlike fmaxf it needs no canonicalising copy of its operands.
+// Maxima (of score rows, and the running ones) use IEEE maximum (v_maximum / v_maximum3):
+// with no NaN in the scores it equals fmaxf, and unlike fmaxf it needs no canonicalising
+// copy of its operands.
 __device__ __forceinline__ float fmax_row(float a, float b) { return __builtin_elementwise_maximum(a, b); }
 
 __device__ __forceinline__ float row_max(const f32x16 (&st)[2]) {
@@ -388,7 +389,7 @@ struct RowState {
 
 // Lazy rescale at the start of a kept tile with row max m_hat (log2 units).
 __device__ __forceinline__ void rescale_if_needed(RowState& rs, f32x16 (&o)[4], float m_hat) {
-  rs.m_true = fmaxf(rs.m_true, m_hat);
+  rs.m_true = fmax_row(rs.m_true, m_hat);
   const bool need = m_hat > rs.m_ref + kRescaleSlack;
   if (__ballot(need) != 0) {
     const float m_new = need ? m_hat : rs.m_ref;
@@ -899,7 +900,7 @@ __device__ __forceinline__ void pair_first_step(int j, const f32x16 (&s_cur)[2],
     skipped_tile(s_next, sm.k[nb], qf, cx.r, cx.g);
   // Keys past the end (a partial last tile, or no second tile at all) do not count.
   if ((tj + 2) * kTK > cx.N) mask_tail(s_next, (tj + 1) * kTK, cx.N, cx.g);
-  const float mhat_pair = fmaxf(mhat, row_max(s_next) * cx.c);
+  const float mhat_pair = fmax_row(mhat, row_max(s_next) * cx.c);
   if constexpr (RULE != kRuleDense) {
     const bool wave_keeps = __ballot(row_keeps<RULE>(rs, mhat_pair, cx.thr_row)) != 0;
     if (cx.lane == 0) sm.vote[0][cx.w] = wave_keeps ? 1 : 0;
@@ -1115,10 +1116,10 @@ __device__ __forceinline__ uint32_t half_votes(const RowState& rs, const float (
   float ref, ref1;
   if constexpr (RULE == kRuleDynSparse) {
     ref = rs.m_ref + log2_fast(half_sum(rs.l_half));
-    ref1 = fmaxf(ref, mh[0] + 5.0f) + 1.0625f;
+    ref1 = fmax_row(ref, mh[0] + 5.0f) + 1.0625f;
   } else {
     ref = rs.m_true;
-    ref1 = fmaxf(rs.m_true, mh[0]);
+    ref1 = fmax_row(rs.m_true, mh[0]);
   }
   const bool k0 = !(mh[0] - ref < cx.thr_row);
   const bool k1 = !(mh[1] - ref < cx.thr_row);
@@ -1168,8 +1169,8 @@ __device__ __forceinline__ void half_tile_step(int j, const f32x16 (&s_cur)[2],
   if (keep0 || keep1_pre) {
     // h0 kept (h1 decided below), or h0 skipped and h1 kept: one body, h0's elements
     // relative to -inf in the second case.
-    raise_reference(rs, o, keep0 ? fmaxf(mh[0], mh[1]) : mh[1]);
-    if (keep0) rs.m_true = fmaxf(rs.m_true, mh[0]);
+    raise_reference(rs, o, keep0 ? fmax_row(mh[0], mh[1]) : mh[1]);
+    if (keep0) rs.m_true = fmax_row(rs.m_true, mh[0]);
     if constexpr (Q8)
       qk_softmax_halves_q8(s_cur, cx.c, keep0 ? -rs.m_ref : -__builtin_inff(), -rs.m_ref,
                            psum0, psum1, pf, va, s_next,
@@ -1211,7 +1212,7 @@ __device__ __forceinline__ void half_tile_step(int j, const f32x16 (&s_cur)[2],
     }
     if (keep1) {
       rs.l_half += psum1;
-      rs.m_true = fmaxf(rs.m_true, mh[1]);
+      rs.m_true = fmax_row(rs.m_true, mh[1]);
       sched_fence();
       pv_second_half(o, pf, va, sm.v[j & 1], cx.lane);
     }
