@@ -33,9 +33,9 @@
 // buffer range check); V is fetched only for tiles that follow a kept tile or are
 // themselves kept, so runs of skipped tiles stream K alone.  Inside an iteration the
 // instruction order is fixed by scheduling fences: the 16 S_{j+1} MFMAs carry 24 elements
-// of the tile-j softmax and the first eight P V MFMAs the other 8 (the ones the last four
-// P V MFMAs read); the row sum is added after the P V MFMAs, where the VALU is otherwise
-// idle; MFMA operands are read from LDS two MFMAs ahead.
+// of the tile-j softmax, the first eight P V MFMAs the other 8 (the ones the last four
+// P V MFMAs read) and the last eight the row max of S_{j+1}; the row sum is added after the
+// P V MFMAs; MFMA operands are read from LDS two MFMAs ahead.
 //
 // Variants, all compile-time parameters of fa_fwd_kernel:
 //   * UNIT: the query rows that share a decision, the workgroup's 128 or each wave's 32;
