@@ -1073,26 +1073,53 @@ __device__ __forceinline__ void qk_softmax_halves_q8(const f32x16 (&s_cur)[2], f
   __builtin_amdgcn_s_setprio(0);
 }
 
+// Lane-local maxima of the two 32-key blocks of a score tile: elements 1 + 2k and 2 + 2k
+// of each block (k = 0..7; element 0 starts each chain), for P.V MFMA slots that carry no
+// other VALU work.  block_max_join completes them.
+__device__ __forceinline__ void block_max_part(const f32x16 (&st)[2], int k, float (&bm)[2]) {
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    if (k == 0) bm[b] = st[b][0];
+#pragma unroll
+    for (int v = 1 + 2 * k; v <= 2 + 2 * k && v < 16; ++v) bm[b] = fmax_row(bm[b], st[b][v]);
+  }
+}
+
 // O += P V_j for the first key half (MFMAs 0-7, keys 0-31; va holds the operands of MFMAs
-// 0 and 1 on entry, those of 8 and 9 on exit) and for the second (MFMAs 8-15).
+// 0 and 1 on entry, those of 8 and 9 on exit) and for the second (MFMAs 8-15).  With MAX
+// the eight MFMAs also carry the lane-local block maxima of st.
+template <bool MAX = false>
 __device__ __forceinline__ void pv_first_half(f32x16 (&o)[4], const bf16x8 (&pf)[4],
-                                              bf16x8 (&va)[3], const uint16_t* vt, int lane) {
+                                              bf16x8 (&va)[3], const uint16_t* vt, int lane,
+                                              const f32x16 (&st)[2], float (&bm)[2]) {
   __builtin_amdgcn_s_setprio(1);
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     va[(i + 2) % 3] = v_operand(vt, i + 2, lane);
     o[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i % 3], pf[i >> 2], o[i & 3], 0, 0, 0);
+    if constexpr (MAX) {
+      block_max_part(st, i, bm);
+      pin_here(bm[0]);
+      pin_here(bm[1]);
+    }
     sched_fence();
   }
   __builtin_amdgcn_s_setprio(0);
 }
+template <bool MAX = false>
 __device__ __forceinline__ void pv_second_half(f32x16 (&o)[4], const bf16x8 (&pf)[4],
-                                               bf16x8 (&va)[3], const uint16_t* vt, int lane) {
+                                               bf16x8 (&va)[3], const uint16_t* vt, int lane,
+                                               const f32x16 (&st)[2], float (&bm)[2]) {
   __builtin_amdgcn_s_setprio(1);
 #pragma unroll
   for (int i = 8; i < 16; ++i) {
     if (i + 2 < 16) va[(i + 2) % 3] = v_operand(vt, i + 2, lane);
     o[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i % 3], pf[i >> 2], o[i & 3], 0, 0, 0);
+    if constexpr (MAX) {
+      block_max_part(st, i - 8, bm);
+      pin_here(bm[0]);
+      pin_here(bm[1]);
+    }
     sched_fence();
   }
   __builtin_amdgcn_s_setprio(0);
@@ -1166,6 +1193,7 @@ __device__ __forceinline__ void half_tile_step(int j, const f32x16 (&s_cur)[2],
   bool keep1 = false;
   bf16x8 pf[4], va[3];
   float psum0 = 0.f, psum1 = 0.f;
+  float bm[2];   // lane-local block maxima of S_{j+1}
   if (keep0 || keep1_pre) {
     // h0 kept (h1 decided below), or h0 skipped and h1 kept: one body, h0's elements
     // relative to -inf in the second case.
@@ -1193,7 +1221,7 @@ __device__ __forceinline__ void half_tile_step(int j, const f32x16 (&s_cur)[2],
         if (UNIT == kTQ && cx.lane == 0) sm.vote_mid[cx.w] = own1 ? 1 : 0;
       }
       sched_fence();
-      pv_first_half(o, pf, va, sm.v[j & 1], cx.lane);   // under the vote exchange
+      pv_first_half<true>(o, pf, va, sm.v[j & 1], cx.lane, s_next, bm);  // under the vote exchange
       if constexpr (RULE != kRuleDense) {
         keep1 = sure1;
         if (exact) {
@@ -1209,12 +1237,14 @@ __device__ __forceinline__ void half_tile_step(int j, const f32x16 (&s_cur)[2],
     } else {
       va[8 % 3] = v_operand(sm.v[j & 1], 8, cx.lane);
       va[9 % 3] = v_operand(sm.v[j & 1], 9, cx.lane);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) block_max_part(s_next, k, bm);
     }
     if (keep1) {
       rs.l_half += psum1;
       rs.m_true = fmax_row(rs.m_true, mh[1]);
       sched_fence();
-      pv_second_half(o, pf, va, sm.v[j & 1], cx.lane);
+      pv_second_half(o, pf, va, sm.v[j & 1], cx.lane, s_next, bm);
     }
   } else {
     if constexpr (Q8)
@@ -1222,6 +1252,8 @@ __device__ __forceinline__ void half_tile_step(int j, const f32x16 (&s_cur)[2],
                       cx.g);
     else
       skipped_tile(s_next, sm.k[nb], qf, cx.r, cx.g);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) block_max_part(s_next, k, bm);
   }
   keep1 = keep1 && h1_exists;
   if (cx.mask_row != nullptr && (UNIT == kTQ ? cx.w == 0 : true) && cx.lane == 0) {
@@ -1240,9 +1272,13 @@ __device__ __forceinline__ void half_tile_step(int j, const f32x16 (&s_cur)[2],
 
   bool next_own0 = true, next_own1 = true, next_s1 = true;
   if (has_next) {
-    if (cx.ragged && j + 1 == cx.n_kt - 1) mask_tail(s_next, (j + 1) * kTK, cx.N, cx.g);
-    mh[0] = block_max(s_next[0]) * cx.c;
-    mh[1] = block_max(s_next[1]) * cx.c;
+    if (cx.ragged && j + 1 == cx.n_kt - 1) {
+      mask_tail(s_next, (j + 1) * kTK, cx.N, cx.g);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) block_max_part(s_next, k, bm);
+    }
+    mh[0] = row_max_join(bm[0]) * cx.c;
+    mh[1] = row_max_join(bm[1]) * cx.c;
     if constexpr (RULE != kRuleDense) {
       const uint32_t b = half_votes<RULE>(rs, mh, cx);
       next_own0 = (b & 1u) != 0;
