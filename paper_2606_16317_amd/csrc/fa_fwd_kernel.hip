@@ -1086,9 +1086,9 @@ __device__ __forceinline__ void block_max_part(const f32x16 (&st)[2], int k, flo
 }
 
 // O += P V_j for the first key half (MFMAs 0-7, keys 0-31; va holds the operands of MFMAs
-// 0 and 1 on entry, those of 8 and 9 on exit) and for the second (MFMAs 8-15).  With MAX
-// the eight MFMAs also carry the lane-local block maxima of st.
-template <bool MAX = false>
+// 0 and 1 on entry, those of 8 and 9 on exit) and for the second (MFMAs 8-15).  The first
+// half's eight MFMAs also carry the lane-local block maxima of st (S_{j+1}); the pins keep
+// the compiler from merging them with the other paths' copies behind the MFMAs.
 __device__ __forceinline__ void pv_first_half(f32x16 (&o)[4], const bf16x8 (&pf)[4],
                                               bf16x8 (&va)[3], const uint16_t* vt, int lane,
                                               const f32x16 (&st)[2], float (&bm)[2]) {
@@ -1097,29 +1097,20 @@ __device__ __forceinline__ void pv_first_half(f32x16 (&o)[4], const bf16x8 (&pf)
   for (int i = 0; i < 8; ++i) {
     va[(i + 2) % 3] = v_operand(vt, i + 2, lane);
     o[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i % 3], pf[i >> 2], o[i & 3], 0, 0, 0);
-    if constexpr (MAX) {
-      block_max_part(st, i, bm);
-      pin_here(bm[0]);
-      pin_here(bm[1]);
-    }
+    block_max_part(st, i, bm);
+    pin_here(bm[0]);
+    pin_here(bm[1]);
     sched_fence();
   }
   __builtin_amdgcn_s_setprio(0);
 }
-template <bool MAX = false>
 __device__ __forceinline__ void pv_second_half(f32x16 (&o)[4], const bf16x8 (&pf)[4],
-                                               bf16x8 (&va)[3], const uint16_t* vt, int lane,
-                                               const f32x16 (&st)[2], float (&bm)[2]) {
+                                               bf16x8 (&va)[3], const uint16_t* vt, int lane) {
   __builtin_amdgcn_s_setprio(1);
 #pragma unroll
   for (int i = 8; i < 16; ++i) {
     if (i + 2 < 16) va[(i + 2) % 3] = v_operand(vt, i + 2, lane);
     o[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i % 3], pf[i >> 2], o[i & 3], 0, 0, 0);
-    if constexpr (MAX) {
-      block_max_part(st, i - 8, bm);
-      pin_here(bm[0]);
-      pin_here(bm[1]);
-    }
     sched_fence();
   }
   __builtin_amdgcn_s_setprio(0);
@@ -1221,7 +1212,7 @@ __device__ __forceinline__ void half_tile_step(int j, const f32x16 (&s_cur)[2],
         if (UNIT == kTQ && cx.lane == 0) sm.vote_mid[cx.w] = own1 ? 1 : 0;
       }
       sched_fence();
-      pv_first_half<true>(o, pf, va, sm.v[j & 1], cx.lane, s_next, bm);  // under the vote exchange
+      pv_first_half(o, pf, va, sm.v[j & 1], cx.lane, s_next, bm);  // under the vote exchange
       if constexpr (RULE != kRuleDense) {
         keep1 = sure1;
         if (exact) {
@@ -1244,7 +1235,7 @@ __device__ __forceinline__ void half_tile_step(int j, const f32x16 (&s_cur)[2],
       rs.l_half += psum1;
       rs.m_true = fmax_row(rs.m_true, mh[1]);
       sched_fence();
-      pv_second_half(o, pf, va, sm.v[j & 1], cx.lane, s_next, bm);
+      pv_second_half(o, pf, va, sm.v[j & 1], cx.lane);
     }
   } else {
     if constexpr (Q8)
