@@ -973,9 +973,12 @@ __device__ __forceinline__ void pair_second_step(int j, const f32x16 (&s_cur)[2]
 // h1 is voted against the LSE after h0:
 //   * if h0 is skipped that LSE is the same, so h1 is voted together with h0;
 //   * if h0 is kept, the step computes the softmax of both halves under the MFMAs of
-//     S_{j+1} (h1 speculatively, its row sum kept apart), adds h0's sum, votes on h1 (an
-//     LDS exchange and a barrier for 128-row units, the wave alone for 32-row units) and
-//     then adds h1's sum and issues h1's eight P.V MFMAs only if h1 is kept.
+//     S_{j+1} (h1 speculatively, its row sum kept apart), adds h0's sum, takes h1's
+//     decision (from the certain-keep bit voted with h0 when some row holds it, see
+//     half_votes; otherwise voted here, with an LDS exchange and a barrier for 128-row
+//     units, the wave alone for 32-row units) and then adds h1's sum and issues h1's
+//     eight P.V MFMAs only if h1 is kept.  h0's eight P.V MFMAs carry the lane-local
+//     block maxima of S_{j+1}; the other paths take them after their MFMAs.
 // The lazy reference max is raised to the larger half max of the tile whenever the tile
 // is entered with a kept half; a half skipped after that only lowers P of the other half
 // by a bounded factor (its max is below the LSE), never the LSE itself.
