@@ -243,13 +243,18 @@ def test_reordered_entry_point_identity_maps(peaked, tk):
 @pytest.mark.parametrize("tk", KEY_TILES)
 def test_wan720p_sampled_tiles(tk):
     q, k, v, _ = workload_inputs("wan720p")
-    announce(f"tile_k={tk} wan720p sampled, lambda=-6 and recall 0.95")
+    announce(f"tile_k={tk} wan720p sampled, lambda=-6, recall 0.95, BLASST 1e-2")
     dev = upload(q, k, v)
     B, H, N, d = q.shape
-    tiles = sample_tiles(B, H, N, per_head=3, heads=[(0, 0), (0, 21)], seed=4)
-    for rule, param in (("dynsparse_lambda", -6.0), ("dynsparse_recall", 0.95)):
-        g = run_gpu(*dev, rule, param, SCALE, tile_k=tk)
-        rep = compare(q, k, v, g, rule, param, SCALE, tiles=tiles, tile_k=tk)
+    cases = [("dynsparse_lambda", -6.0, 128), ("dynsparse_recall", 0.95, 128),
+             ("blasst", 1e-2, 128)]
+    if tk == 32:   # each wave's 32 rows deciding alone: the mid-step vote without a barrier
+        cases.append(("dynsparse_lambda", -6.0, 32))
+    for rule, param, tq in cases:
+        announce(f"tile_k={tk} tile_q={tq} rule={rule} param={param}")
+        tiles = sample_tiles(B, H, N, per_head=3, heads=[(0, 0), (0, 21)], seed=4, tile_q=tq)
+        g = run_gpu(*dev, rule, param, SCALE, tile_q=tq, tile_k=tk)
+        rep = compare(q, k, v, g, rule, param, SCALE, tiles=tiles, tile_q=tq, tile_k=tk)
         print(rep, flush=True)
         assert_parity(rep)
-        assert (g.stats == expected_stats_from_mask(g.mask, N, 128, tk)).all()
+        assert (g.stats == expected_stats_from_mask(g.mask, N, tq, tk)).all()
